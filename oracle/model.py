@@ -129,16 +129,23 @@ def layer_forward(x: np.ndarray, lw: dict, cfg, cos, sin, allowed, act_round=Non
     return x + a @ f64(lw["w_down"]).T
 
 
-def forward_hidden(weights: dict, cfg, tokens, pos, allowed, act_round=None,
-                   n_layers: int | None = None) -> np.ndarray:
-    """Final-normed hidden states [T, d] for token ids ``tokens`` [T]."""
-    rnd = act_round or (lambda a: a)
+def forward_residual(weights: dict, cfg, tokens, pos, allowed, act_round=None,
+                     n_layers: int | None = None) -> np.ndarray:
+    """Residual stream [T, d] after the embedding and the first n_layers layers."""
     tokens = np.asarray(tokens, dtype=np.int64)
     x = f64(weights["tok_emb"][torch.as_tensor(tokens)])
     cos, sin = rope_cos_sin(pos, cfg.head_dim, cfg.rope_theta)
     nl = cfg.n_layers if n_layers is None else n_layers
     for layer in range(nl):
         x = layer_forward(x, weights["layers"][layer], cfg, cos, sin, allowed, act_round)
+    return x
+
+
+def forward_hidden(weights: dict, cfg, tokens, pos, allowed, act_round=None,
+                   n_layers: int | None = None) -> np.ndarray:
+    """Final-normed hidden states [T, d] for token ids ``tokens`` [T]."""
+    rnd = act_round or (lambda a: a)
+    x = forward_residual(weights, cfg, tokens, pos, allowed, act_round, n_layers)
     return rnd(rmsnorm(x, f64(weights["final_norm"]), cfg.rms_eps))
 
 

@@ -1,0 +1,257 @@
+// WINO decision on device.
+//
+// epi_stats_kernel: for the standalone epilogue, each workgroup streams one
+//   chunk of one needed logits row (the current row of a masked position, the
+//   shadow row of an unmasked one) and writes partial softmax statistics.
+// decide_kernel: one workgroup per sequence merges the partials of its block
+//   positions (log-sum-exp merge; best non-mask id with lowest-id ties), turns
+//   them into the draft confidence (Eq. 2) or the verify probability (Eq. 3),
+//   and applies Eq. 4 with the forced draft (Eq. 1) and the step cap.
+#include <climits>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace wino {
+namespace {
+
+struct RowStats {  // layout of wino_row_stats
+  float m_all, sumexp, z_best, z_target;
+  int32_t argmax, row_kind;
+};
+
+struct Part {
+  float m, s, b, t;
+  int i;
+};
+
+__device__ __forceinline__ void merge(Part& a, const Part& o) {
+  const float m = fmaxf(a.m, o.m);
+  a.s = a.s * __expf(a.m - m) + o.s * __expf(o.m - m);
+  a.m = m;
+  if (o.b > a.b || (o.b == a.b && o.i < a.i)) { a.b = o.b; a.i = o.i; }
+  a.t = fmaxf(a.t, o.t);
+}
+
+__device__ __forceinline__ Part wave_merge(Part p) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    Part q;
+    q.m = __shfl_xor(p.m, o, 64);
+    q.s = __shfl_xor(p.s, o, 64);
+    q.b = __shfl_xor(p.b, o, 64);
+    q.t = __shfl_xor(p.t, o, 64);
+    q.i = __shfl_xor(p.i, o, 64);
+    merge(p, q);
+  }
+  return p;
+}
+
+__global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
+  extern __shared__ int smem_i[];
+  int* s_cur = smem_i;                                   // [Lb] token before the step
+  float* s_val = reinterpret_cast<float*>(s_cur + a.Lb);  // [Lb] conf (masked) or s (unmasked)
+  int* s_hat = reinterpret_cast<int*>(s_val + a.Lb);      // [Lb] draft id
+  int* s_flag = s_hat + a.Lb;                             // [Lb] decision
+  __shared__ int s_nmask, s_nmask_after, s_any_draft, s_forced;
+
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int Lb = a.Lb;
+  RowStats* stats = reinterpret_cast<RowStats*>(a.stats);
+
+  int32_t* cur_ptr;
+  bool done = false;
+  if (a.standalone) {
+    cur_ptr = a.tokens + (size_t)b * Lb;
+  } else {
+    const int bs = a.block_start[b];
+    done = bs >= a.G;
+    // same clamping as the forward kernels: Y_cur always lies inside the response
+    const int bsc = bs < 0 ? 0 : (bs > a.G - Lb ? a.G - Lb : bs);
+    cur_ptr = a.tokens + (size_t)b * a.S + a.P + bsc;
+  }
+  if (tid == 0) { s_nmask = 0; s_nmask_after = 0; s_any_draft = 0; s_forced = -1; }
+  __syncthreads();
+  if (!done) {
+    for (int l = tid; l < Lb; l += 256) {
+      const int t = cur_ptr[l];
+      s_cur[l] = t;
+      if (t == a.mask_id) atomicAdd(&s_nmask, 1);
+    }
+  }
+  __syncthreads();
+  // A finished sequence, or (fused step) a block with no mask left, is idle.
+  const bool idle = done || (!a.standalone && s_nmask == 0);
+  if (idle) {
+    for (int l = tid; l < Lb; l += 256) {
+      if (a.flags) a.flags[(size_t)b * Lb + l] = WINO_KEEP_FLAG;
+      if (a.bitmap) a.bitmap[(size_t)b * Lb + l] = done ? 0 : (s_cur[l] == a.mask_id);
+      if (stats) {
+        RowStats z = {0.f, 0.f, 0.f, 0.f, -1, -1};
+        stats[(size_t)b * Lb + l] = z;
+      }
+    }
+    if (tid == 0 && a.n_masked) a.n_masked[b] = 0;
+    return;
+  }
+
+  // merge partials: one wave per position
+  for (int l = wave; l < Lb; l += 4) {
+    const size_t row = (size_t)b * Lb + l;
+    Part p = {kNegBig, 0.f, kNegBig, kNegBig, INT_MAX};
+    for (int j = lane; j < a.n_part; j += 64) {
+      const size_t o = row * a.n_part + j;
+      Part q = {a.pm[o], a.ps[o], a.pb[o], a.pt[o], a.pi[o]};
+      merge(p, q);
+    }
+    p = wave_merge(p);
+    if (lane == 0) {
+      const bool masked = s_cur[l] == a.mask_id;
+      const float z = masked ? p.b : p.t;
+      s_val[l] = __expf(z - p.m) / p.s;  // Eq. 2 confidence / Eq. 3 probability
+      s_hat[l] = p.i;
+      if (stats) {
+        RowStats r = {p.m, p.s, p.b, masked ? kNegBig : p.t, p.i, masked ? 0 : 1};
+        stats[row] = r;
+      }
+    }
+  }
+  __syncthreads();
+
+  const int steps_before = (!a.standalone && a.block_steps) ? a.block_steps[b] : 0;
+  const bool cap_now = !a.standalone && a.cap_fill && (steps_before + 1 >= a.cap);
+  for (int l = tid; l < Lb; l += 256) {
+    const bool masked = s_cur[l] == a.mask_id;
+    int f = WINO_KEEP_FLAG;
+    if (masked) {
+      if (cap_now) f = WINO_CAPFILL_FLAG;
+      else if (s_val[l] > a.tau1) { f = WINO_DRAFT_FLAG; s_any_draft = 1; }
+    } else if (!cap_now && s_val[l] < a.tau2) {
+      f = WINO_REMASK_FLAG;
+    }
+    s_flag[l] = f;
+  }
+  __syncthreads();
+  if (tid == 0 && !cap_now && a.force_top1 && s_nmask > 0 && !s_any_draft) {
+    // Eq. 1: the most confident masked position (lowest position on ties)
+    int best = -1;
+    float bv = 0.f;
+    for (int l = 0; l < Lb; ++l)
+      if (s_cur[l] == a.mask_id && (best < 0 || s_val[l] > bv)) { best = l; bv = s_val[l]; }
+    s_flag[best] = WINO_FORCED_FLAG;
+  }
+  __syncthreads();
+  for (int l = tid; l < Lb; l += 256) {
+    const int f = s_flag[l];
+    int t = s_cur[l];
+    if (f == WINO_DRAFT_FLAG || f == WINO_FORCED_FLAG || f == WINO_CAPFILL_FLAG) t = s_hat[l];
+    else if (f == WINO_REMASK_FLAG) t = a.mask_id;
+    if (t != s_cur[l]) cur_ptr[l] = t;
+    if (t == a.mask_id) atomicAdd(&s_nmask_after, 1);
+    if (a.flags) a.flags[(size_t)b * Lb + l] = (uint8_t)f;
+    if (a.bitmap) a.bitmap[(size_t)b * Lb + l] = t == a.mask_id;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    if (a.n_masked) a.n_masked[b] = s_nmask_after;
+    if (a.seq_steps) a.seq_steps[b] += 1;
+    if (!a.standalone && a.block_steps) a.block_steps[b] = steps_before + 1;
+    if (!a.standalone && a.advance && s_nmask_after == 0) {
+      a.block_start[b] += Lb;
+      if (a.block_steps) a.block_steps[b] = 0;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void epi_stats_kernel(const uint16_t* __restrict__ logits,
+                                                        const int32_t* __restrict__ cur, int Lb, int V,
+                                                        int mask_id, float* pm, float* ps, float* pb,
+                                                        int32_t* pi, float* pt, int n_part) {
+  constexpr int IT = kEpiChunk / (256 * 8);
+  __shared__ float red[4][4];
+  __shared__ int redi[4];
+  const int r = blockIdx.y, chunk = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int b = r / Lb, l = r - b * Lb;
+  const int tok = cur[r];
+  const bool masked = tok == mask_id;
+  const uint16_t* row = logits + ((size_t)b * 2 * Lb + (masked ? l : Lb + l)) * V;
+  const int tgt = masked ? -1 : tok;
+  const int v0 = chunk * kEpiChunk;
+  const int v1 = min(V, v0 + kEpiChunk);
+
+  uint4 raw[IT];
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int idx = v0 + (it * 256 + tid) * 8;
+    raw[it] = idx < v1 ? *reinterpret_cast<const uint4*>(row + idx) : make_uint4(0, 0, 0, 0);
+  }
+  float mx = kNegBig, bz = kNegBig, tz = kNegBig;
+  int bi = INT_MAX;
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int idx = v0 + (it * 256 + tid) * 8;
+    if (idx >= v1) continue;
+    const uint16_t* p = reinterpret_cast<const uint16_t*>(&raw[it]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float z = bf2f(p[e]);
+      mx = fmaxf(mx, z);
+      if (idx + e != mask_id && z > bz) { bz = z; bi = idx + e; }
+      if (idx + e == tgt) tz = z;
+    }
+  }
+  // block max
+  float m = wave_max(mx);
+  if (lane == 0) red[0][wave] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
+  float se = 0.f;
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int idx = v0 + (it * 256 + tid) * 8;
+    if (idx >= v1) continue;
+    const uint16_t* p = reinterpret_cast<const uint16_t*>(&raw[it]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) se += __expf(bf2f(p[e]) - m);
+  }
+  se = wave_sum(se);
+  tz = wave_max(tz);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ob = __shfl_xor(bz, o, 64);
+    const int oi = __shfl_xor(bi, o, 64);
+    if (ob > bz || (ob == bz && oi < bi)) { bz = ob; bi = oi; }
+  }
+  if (lane == 0) { red[1][wave] = se; red[2][wave] = bz; red[3][wave] = tz; redi[wave] = bi; }
+  __syncthreads();
+  if (tid == 0) {
+    float s = 0.f, bb = kNegBig, tt = kNegBig;
+    int ii = INT_MAX;
+    for (int w = 0; w < 4; ++w) {
+      s += red[1][w];
+      tt = fmaxf(tt, red[3][w]);
+      if (red[2][w] > bb || (red[2][w] == bb && redi[w] < ii)) { bb = red[2][w]; ii = redi[w]; }
+    }
+    const size_t o = (size_t)r * n_part + chunk;
+    pm[o] = m; ps[o] = s; pb[o] = bb; pi[o] = ii; pt[o] = tt;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_decide(const DecideArgs& a, hipStream_t st) {
+  const size_t shm = (size_t)a.Lb * 16;
+  decide_kernel<<<a.B, 256, shm, st>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_epilogue_stats(const uint16_t* logits, const int32_t* cur_tokens, int B, int Lb,
+                                 int V, int mask_id, float* pm, float* ps, float* pb, int32_t* pi,
+                                 float* pt, hipStream_t st) {
+  const int n_part = (V + kEpiChunk - 1) / kEpiChunk;
+  dim3 grid(n_part, B * Lb);
+  epi_stats_kernel<<<grid, 256, 0, st>>>(logits, cur_tokens, Lb, V, mask_id, pm, ps, pb, pi, pt, n_part);
+  return hipGetLastError();
+}
+
+}  // namespace wino

@@ -1,0 +1,168 @@
+// Embedding gather and RMSNorm kernels: one wave per row, the row held in
+// registers (16-byte chunks of 8 elements per lane), fp32 sum of squares by a
+// wave butterfly, bf16 output rounded to nearest even.
+#include "common.h"
+#include "kernels.h"
+
+namespace wino {
+
+namespace {
+
+template <int CPL>
+__device__ __forceinline__ void norm_store(float (&v)[CPL][8], float ss, const uint16_t* gain,
+                                           float eps, int d, int lane, uint16_t* out) {
+  const int nch = d >> 3;
+  ss = wave_sum(ss);
+  const float r = rsqrtf(ss / (float)d + eps);
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    const int ch = lane + c * 64;
+    if (ch < nch) {
+      const uint4 graw = *reinterpret_cast<const uint4*>(gain + ch * 8);
+      const uint16_t* gp = reinterpret_cast<const uint16_t*>(&graw);
+      uint4 o;
+      uint32_t* op = reinterpret_cast<uint32_t*>(&o);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        op[e] = pack2bf(v[c][2 * e] * r * bf2f(gp[2 * e]), v[c][2 * e + 1] * r * bf2f(gp[2 * e + 1]));
+      *reinterpret_cast<uint4*>(out + ch * 8) = o;
+    }
+  }
+}
+
+template <int CPL>
+__global__ __launch_bounds__(256) void embed_norm_kernel(StepGeom g, const int32_t* __restrict__ tokens,
+                                                         const uint16_t* __restrict__ emb, int vocab,
+                                                         const uint16_t* __restrict__ gain, float eps,
+                                                         int d, float* __restrict__ x,
+                                                         uint16_t* __restrict__ h) {
+  const int lane = threadIdx.x & 63;
+  const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (m >= g.B * g.T) return;
+  const int b = m / g.T, t = m - b * g.T;
+  int tok = t < g.S ? tokens[(size_t)b * g.S + t] : g.mask_id;
+  tok = tok < 0 ? 0 : (tok >= vocab ? vocab - 1 : tok);  // ids outside [0,V) are clamped
+  const uint16_t* src = emb + (size_t)tok * d;
+  float* xr = x + (size_t)m * d;
+  const int nch = d >> 3;
+  float v[CPL][8];
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    const int ch = lane + c * 64;
+    if (ch < nch) {
+      const uint4 raw = *reinterpret_cast<const uint4*>(src + ch * 8);
+      const uint16_t* p = reinterpret_cast<const uint16_t*>(&raw);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        v[c][e] = bf2f(p[e]);
+        ss += v[c][e] * v[c][e];
+      }
+      float4* xo = reinterpret_cast<float4*>(xr + ch * 8);
+      xo[0] = make_float4(v[c][0], v[c][1], v[c][2], v[c][3]);
+      xo[1] = make_float4(v[c][4], v[c][5], v[c][6], v[c][7]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[c][e] = 0.f;
+    }
+  }
+  norm_store<CPL>(v, ss, gain, eps, d, lane, h + (size_t)m * d);
+}
+
+template <int CPL>
+__device__ __forceinline__ float load_row_f32(const float* xr, int d, int lane, float (&v)[CPL][8]) {
+  const int nch = d >> 3;
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    const int ch = lane + c * 64;
+    if (ch < nch) {
+      const float4* xi = reinterpret_cast<const float4*>(xr + ch * 8);
+      const float4 a = xi[0], bq = xi[1];
+      v[c][0] = a.x; v[c][1] = a.y; v[c][2] = a.z; v[c][3] = a.w;
+      v[c][4] = bq.x; v[c][5] = bq.y; v[c][6] = bq.z; v[c][7] = bq.w;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss += v[c][e] * v[c][e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[c][e] = 0.f;
+    }
+  }
+  return ss;
+}
+
+template <int CPL>
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ x,
+                                                      const uint16_t* __restrict__ gain, float eps,
+                                                      int M, int d, uint16_t* __restrict__ h) {
+  const int lane = threadIdx.x & 63;
+  const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (m >= M) return;
+  float v[CPL][8];
+  const float ss = load_row_f32<CPL>(x + (size_t)m * d, d, lane, v);
+  norm_store<CPL>(v, ss, gain, eps, d, lane, h + (size_t)m * d);
+}
+
+template <int CPL>
+__global__ __launch_bounds__(256) void select_norm_kernel(StepGeom g, int mode,
+                                                          const int32_t* __restrict__ tokens,
+                                                          const float* __restrict__ x,
+                                                          const uint16_t* __restrict__ gain,
+                                                          float eps, int d, uint16_t* __restrict__ hf,
+                                                          int32_t* __restrict__ target) {
+  const int lane = threadIdx.x & 63;
+  const int rows_per_seq = mode == 0 ? g.Lb : 2 * g.Lb;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= g.B * rows_per_seq) return;
+  const int b = r / rows_per_seq, j = r - b * rows_per_seq;
+  const int c0 = cur_start(g, b);
+  int src;
+  if (mode == 0) {
+    const int tok = tokens[(size_t)b * g.S + c0 + j];
+    const bool masked = tok == g.mask_id;
+    src = masked ? c0 + j : g.S + j;  // Eq. 4: draft reads Y_cur, verify reads Y_shad
+    if (lane == 0) target[r] = masked ? -1 : tok;
+  } else {
+    src = j < g.Lb ? c0 + j : g.S + (j - g.Lb);
+    if (lane == 0) target[r] = -1;
+  }
+  float v[CPL][8];
+  const float ss = load_row_f32<CPL>(x + ((size_t)b * g.T + src) * d, d, lane, v);
+  norm_store<CPL>(v, ss, gain, eps, d, lane, hf + (size_t)r * d);
+}
+
+}  // namespace
+
+// The library accepts d <= 4096 (up to 8 chunks of 8 elements per lane).
+void launch_embed_norm(const StepGeom& g, const int32_t* tokens, const uint16_t* emb, int vocab,
+                       const uint16_t* gain, float eps, int d, float* x, uint16_t* h,
+                       hipStream_t st) {
+  const int M = g.B * g.T;
+  dim3 grid((M + 3) / 4), block(256);
+  if (d <= 512) embed_norm_kernel<1><<<grid, block, 0, st>>>(g, tokens, emb, vocab, gain, eps, d, x, h);
+  else if (d <= 1024) embed_norm_kernel<2><<<grid, block, 0, st>>>(g, tokens, emb, vocab, gain, eps, d, x, h);
+  else if (d <= 2048) embed_norm_kernel<4><<<grid, block, 0, st>>>(g, tokens, emb, vocab, gain, eps, d, x, h);
+  else embed_norm_kernel<8><<<grid, block, 0, st>>>(g, tokens, emb, vocab, gain, eps, d, x, h);
+}
+
+void launch_rmsnorm(const float* x, const uint16_t* gain, float eps, int M, int d, uint16_t* h,
+                    hipStream_t st) {
+  dim3 grid((M + 3) / 4), block(256);
+  if (d <= 512) rmsnorm_kernel<1><<<grid, block, 0, st>>>(x, gain, eps, M, d, h);
+  else if (d <= 1024) rmsnorm_kernel<2><<<grid, block, 0, st>>>(x, gain, eps, M, d, h);
+  else if (d <= 2048) rmsnorm_kernel<4><<<grid, block, 0, st>>>(x, gain, eps, M, d, h);
+  else rmsnorm_kernel<8><<<grid, block, 0, st>>>(x, gain, eps, M, d, h);
+}
+
+void launch_select_norm(const StepGeom& g, int mode, const int32_t* tokens, const float* x,
+                        const uint16_t* gain, float eps, int d, uint16_t* hf, int32_t* target,
+                        hipStream_t st) {
+  const int R = g.B * (mode == 0 ? g.Lb : 2 * g.Lb);
+  dim3 grid((R + 3) / 4), block(256);
+  if (d <= 512) select_norm_kernel<1><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, target);
+  else if (d <= 1024) select_norm_kernel<2><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, target);
+  else if (d <= 2048) select_norm_kernel<4><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, target);
+  else select_norm_kernel<8><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, target);
+}
+
+}  // namespace wino

@@ -1,0 +1,130 @@
+// Launch interface between the host library and the WINO kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace wino {
+
+// Geometry of one step over a batch of independent sequences.  Rows of the
+// extended sequence are ordered [prompt | generation | shadow block]; the
+// residual stream holds B*T rows, row b*T + t.
+struct StepGeom {
+  int B, P, G, Lb;      // batch, prompt length, generation length, block length
+  int S, T, Tp;         // S = P + G, T = S + Lb, Tp = T rounded up to 64
+  int mask_id;
+  const int32_t* block_start;  // [B] generation-relative start of Y_cur
+};
+
+// Absolute index of y_cur,1 for sequence b; finished sequences are clamped to
+// the last block (their outputs are ignored).
+__device__ __forceinline__ int cur_start(const StepGeom& g, int b) {
+  int bs = g.block_start[b];
+  bs = bs < 0 ? 0 : (bs > g.G - g.Lb ? g.G - g.Lb : bs);
+  return g.P + bs;
+}
+
+// Position id of row t (Sec. 4.2.2): shadow row j reuses y_cur,j's id.
+__device__ __forceinline__ int row_pos(const StepGeom& g, int b, int t) {
+  return t < g.S ? t : cur_start(g, b) + (t - g.S);
+}
+
+// --------------------------------------------------------------- elementwise
+// x[m] = E[token of row m] (fp32); h[m] = rmsnorm(x[m]) * gain (bf16).
+void launch_embed_norm(const StepGeom& g, const int32_t* tokens, const uint16_t* emb, int vocab,
+                       const uint16_t* gain, float eps, int d, float* x, uint16_t* h,
+                       hipStream_t st);
+// h[m] = rmsnorm(x[m]) * gain for m < M.
+void launch_rmsnorm(const float* x, const uint16_t* gain, float eps, int M, int d, uint16_t* h,
+                    hipStream_t st);
+// Rows the decision reads.  mode 0: one row per block position (current row
+// if the token is the mask, else the shadow row) and target = current token
+// (-1 for masked).  mode 1: all 2*Lb rows (current then shadow) per sequence.
+void launch_select_norm(const StepGeom& g, int mode, const int32_t* tokens, const float* x,
+                        const uint16_t* gain, float eps, int d, uint16_t* hf, int32_t* target,
+                        hipStream_t st);
+
+// --------------------------------------------------------------- GEMM
+// C = A * W^T with A bf16 [M, K] (row stride lda), W bf16 [N, K] (row stride
+// ldw), fp32 accumulation, and one of the fused epilogues below.
+struct RopeOut {      // QKV projection + rotate-half RoPE, head-major outputs
+  uint16_t* q;        // [B, H, Tp, hd]
+  uint16_t* k;        // [B, H, Tp, hd]
+  uint16_t* vt;       // [B, H, hd, Tp]  (value transposed: token-contiguous)
+  const float* cos_t; // [max_pos, hd/2]
+  const float* sin_t;
+  int H, hd;
+};
+struct LmStatsOut {   // LM head + streaming softmax statistics per (row, N-tile)
+  const float* bias;  // [V] or null
+  const int32_t* target;  // [M] id whose logit is recorded, or -1
+  int mask_id;
+  int n_part;         // partials per row (= N / BN)
+  float* pm;          // [M, n_part] max logit of the tile
+  float* ps;          // [M, n_part] sum exp(z - pm)
+  float* pb;          // [M, n_part] max logit over ids != mask
+  int32_t* pi;        // [M, n_part] lowest id reaching pb
+  float* pt;          // [M, n_part] logit of target (kNegBig if not in tile)
+};
+
+enum GemmEpi { EPI_QKV_ROPE = 0, EPI_RESIDUAL = 1, EPI_SWIGLU = 2, EPI_LMSTATS = 3, EPI_STORE_F32 = 4 };
+
+struct GemmCall {
+  const uint16_t* A; int lda;
+  const uint16_t* W; int ldw;
+  int M, N, K;
+  GemmEpi epi;
+  // residual: x[m*ldc + n] += acc ; store: out[m*ldc + n] = acc (+ bias[n])
+  float* outf; int ldc; const float* bias;
+  // swiglu: out[m*ldc + f] = silu(gate) * up (bf16); W rows: gate [0,F), up [F,2F)
+  uint16_t* outh; int F;
+  RopeOut rope;
+  StepGeom geom;
+  LmStatsOut lm;
+};
+// Picks a tile shape for the problem; returns the N-tile width used (the LM
+// head needs it to size its partials) or 0 if no kernel fits.
+int gemm_tile_n(const GemmCall& c);
+hipError_t launch_gemm(const GemmCall& c, hipStream_t st);
+
+// --------------------------------------------------------------- attention
+// Bidirectional attention with the WINO shadow mask (Sec. 4.2.2): query row
+// t < S sees keys [0, S); shadow query S+j sees keys [0, T) except c0+j.
+// o: bf16 [B*T, H*hd] row-major.
+hipError_t launch_attention(const StepGeom& g, const uint16_t* q, const uint16_t* k,
+                            const uint16_t* vt, int H, int hd, uint16_t* o, hipStream_t st);
+
+// --------------------------------------------------------------- decision
+// Per-position decision codes (same values as the public WINO_* flags).
+constexpr int WINO_KEEP_FLAG = 0, WINO_DRAFT_FLAG = 1, WINO_REMASK_FLAG = 2,
+              WINO_FORCED_FLAG = 3, WINO_CAPFILL_FLAG = 4;
+
+struct DecideArgs {
+  // partial softmax statistics [R, n_part] (R = B*Lb rows, row b*Lb + l)
+  const float* pm; const float* ps; const float* pb; const int32_t* pi; const float* pt;
+  int n_part;
+  int B, Lb, mask_id;
+  float tau1, tau2;
+  int force_top1, cap_fill, cap;
+  // fused-step mode: tokens [B, S] with Y_cur at P + block_start[b]
+  int standalone;       // 1: tokens are [B, Lb] (Y_cur only), Eq. 4 always applied
+  int32_t* tokens; int S, P, G;
+  int32_t* block_start;  // [B]
+  int32_t* block_steps;  // [B] or null
+  int advance;           // move block_start to the next block when Y_cur is full
+  int32_t* seq_steps;    // [B] steps counter or null
+  uint8_t* flags;        // [B, Lb] or null
+  uint8_t* bitmap;       // [B, Lb] or null (standalone)
+  int32_t* n_masked;     // [B] or null
+  void* stats;           // wino_row_stats [B, Lb] or null
+};
+hipError_t launch_decide(const DecideArgs& a, hipStream_t st);
+
+// Standalone epilogue statistics: for each (b, l) pick the current row
+// (masked) or the shadow row (unmasked) of bf16 logits [B, 2Lb, V], and write
+// partials over chunks of kEpiChunk ids.
+constexpr int kEpiChunk = 16384;
+hipError_t launch_epilogue_stats(const uint16_t* logits, const int32_t* cur_tokens, int B, int Lb,
+                                 int V, int mask_id, float* pm, float* ps, float* pb, int32_t* pi,
+                                 float* pt, hipStream_t st);
+
+}  // namespace wino

@@ -1,0 +1,360 @@
+"""Parity of the HIP path (through the C ABI) against the float64 oracle.
+
+Every input is seeded and synthetic; oracle inputs are the same bytes the GPU
+receives.  Tolerances: logits within 2e-2 max relative error per row; decisions
+and token ids bit-exact wherever the oracle's deciding probability is more than
+1e-3 from its threshold (ids also need a top-2 gap above 1e-3).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import wino_inputs as wi
+from oracle import epilogue as E
+from oracle import model as M
+from oracle import wino as W
+from helpers import (LOGIT_TOL, MARGIN, decided_mask, forced_is_robust, rowwise_rel_err, to_cpu,
+                     to_device)
+
+pytestmark = pytest.mark.gpu
+
+STATS_DT = np.dtype([("m_all", "<f4"), ("sumexp", "<f4"), ("z_best", "<f4"), ("z_target", "<f4"),
+                     ("argmax", "<i4"), ("row_kind", "<i4")])
+
+
+@pytest.fixture(scope="module")
+def P():
+    import paper_2605_16941_amd as pkg
+    return pkg
+
+
+def tiny(variant="wide", seed=0, gain_std=0.1, **kw):
+    cfg = wi.preset("tiny", **kw)
+    lhs = wi.wide_lm_head_std(cfg) if variant == "wide" else None
+    return cfg, wi.model_weights(cfg, seed=seed, lm_head_std=lhs, gain_std=gain_std)
+
+
+def batch_tokens(cfg, B, p, g, seed=0, fill=None):
+    pr = wi.prompts(cfg, B, p, seed=seed)
+    tok = wi.initial_tokens(pr, g, cfg.mask_id).numpy().astype(np.int64)
+    if fill:
+        rng = np.random.default_rng(seed)
+        for b in range(B):
+            for (lo, hi, frac) in fill:
+                idx = np.arange(p + lo, p + hi)
+                sel = idx[rng.random(len(idx)) < frac]
+                tok[b, sel] = rng.integers(0, cfg.mask_id, len(sel))
+    return tok
+
+
+def gpu_step(P, model, prm, tokens, block_start, block_steps):
+    B, lb = tokens.shape[0], prm.block_len
+    tok = torch.tensor(tokens, dtype=torch.int32, device="cuda")
+    bs = torch.tensor(block_start, dtype=torch.int32, device="cuda")
+    st = torch.tensor(block_steps, dtype=torch.int32, device="cuda")
+    flags = torch.full((B, lb), 255, dtype=torch.uint8, device="cuda")
+    nm = torch.full((B,), -7, dtype=torch.int32, device="cuda")
+    stats = torch.zeros(B * lb * STATS_DT.itemsize, dtype=torch.uint8, device="cuda")
+    P.wino_step(model.ctx, prm, tok, bs, st, flags, nm, stats)
+    torch.cuda.synchronize()
+    return (tok.cpu().numpy(), flags.cpu().numpy(), nm.cpu().numpy(), st.cpu().numpy(),
+            stats.cpu().numpy().view(STATS_DT).reshape(B, lb))
+
+
+def oracle_params(prm_c, **kw):
+    return W.Params(prm_c.prompt_len, prm_c.gen_len, prm_c.block_len, prm_c.mask_id,
+                    float(np.float32(prm_c.tau1)), float(np.float32(prm_c.tau2)), prm_c.max_steps, **kw)
+
+
+def compare_step(gpu_tok, gpu_flags, r, cur, mask_id, tau1, c0, lb, label=""):
+    """Assert GPU decisions equal the oracle's where the oracle fixes them.
+    Returns how many positions were compared."""
+    masked = cur == mask_id
+    ok = decided_mask(r.margin, r.top2_gap, masked)
+    cap_now = np.any(r.flags == W.CAPFILL)
+    if cap_now:
+        ok = ~masked | (r.top2_gap > MARGIN)
+    else:
+        confm = r.conf[masked]
+        if masked.any() and not np.any(confm > tau1 + MARGIN):
+            if np.all(confm < tau1 - MARGIN) and forced_is_robust(r.conf, masked):
+                pass  # the forced draft is fixed: compare it
+            else:
+                ok &= ~masked
+    n = 0
+    for l in range(lb):
+        if not ok[l]:
+            continue
+        assert gpu_flags[l] == r.flags[l], f"{label} pos {l}: flag {gpu_flags[l]} != {r.flags[l]}"
+        assert gpu_tok[c0 + l] == r.tokens[c0 + l], f"{label} pos {l}: token differs"
+        n += 1
+    return n
+
+
+# ---------------------------------------------------------------- forward pieces
+def test_embedding_rows_are_exact(P):
+    cfg, w = tiny()
+    wd = to_device(w)
+    p, g, lb, B = 32, 64, 16, 2
+    model = P.WinoModel(cfg, wd, B, p + g + lb)
+    tok = batch_tokens(cfg, B, p, g, fill=[(0, 16, 0.5)])
+    prm = P.make_params(B, p, g, lb, cfg.mask_id)
+    out = torch.empty(B, p + g + lb, cfg.d_model, dtype=torch.float32, device="cuda")
+    P.wino_debug_forward(model.ctx, prm, torch.tensor(tok, dtype=torch.int32, device="cuda"),
+                         torch.tensor([0, 16], dtype=torch.int32, device="cuda"), 0, out)
+    torch.cuda.synchronize()
+    ext = np.concatenate([tok, np.full((B, lb), cfg.mask_id)], axis=1)
+    want = w["tok_emb"].float()[torch.from_numpy(ext)]
+    assert torch.equal(out.cpu(), want)
+    model.close()
+
+
+@pytest.mark.parametrize("n_layers", [1, 2])
+def test_residual_stream_matches_oracle(P, n_layers):
+    cfg, w = tiny()
+    wd = to_device(w)
+    p, g, lb, B = 32, 64, 16, 2
+    model = P.WinoModel(cfg, wd, B, p + g + lb)
+    tok = batch_tokens(cfg, B, p, g, fill=[(0, 16, 0.5), (16, 48, 1.0)])
+    bstart = [16, 0]
+    prm = P.make_params(B, p, g, lb, cfg.mask_id)
+    out = torch.empty(B, p + g + lb, cfg.d_model, dtype=torch.float32, device="cuda")
+    P.wino_debug_forward(model.ctx, prm, torch.tensor(tok, dtype=torch.int32, device="cuda"),
+                         torch.tensor(bstart, dtype=torch.int32, device="cuda"), n_layers, out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    for b in range(B):
+        ext, pos, allowed, _ = M.extended_inputs(tok[b], p, g, lb, bstart[b], cfg.mask_id)
+        ref = M.forward_residual(w, cfg, ext, pos, allowed, n_layers=n_layers)
+        err = rowwise_rel_err(got[b], ref)
+        assert err < 1e-2, f"seq {b}: residual rel err {err}"
+    model.close()
+
+
+@pytest.mark.parametrize("variant", ["literal", "wide"])
+def test_logits_match_oracle(P, variant):
+    cfg, w = tiny(variant)
+    wd = to_device(w)
+    p, g, lb, B = 32, 64, 16, 2
+    model = P.WinoModel(cfg, wd, B, p + g + lb)
+    tok = batch_tokens(cfg, B, p, g, seed=3, fill=[(0, 32, 1.0), (32, 48, 0.4)])
+    bstart = [32, 32]
+    prm = P.make_params(B, p, g, lb, cfg.mask_id)
+    logits = torch.empty(B, 2 * lb, cfg.vocab, dtype=torch.float32, device="cuda")
+    P.wino_debug_logits(model.ctx, prm, torch.tensor(tok, dtype=torch.int32, device="cuda"),
+                        torch.tensor(bstart, dtype=torch.int32, device="cuda"), logits)
+    torch.cuda.synchronize()
+    got = logits.cpu().numpy()
+    for b in range(B):
+        ext, pos, allowed, c0 = M.extended_inputs(tok[b], p, g, lb, bstart[b], cfg.mask_id)
+        s = p + g
+        for rnd, tol in ((None, LOGIT_TOL), (M.round_bf16, LOGIT_TOL)):
+            h = M.forward_hidden(w, cfg, ext, pos, allowed, act_round=rnd)
+            ref = np.concatenate([M.lm_logits(w, h[c0:c0 + lb]), M.lm_logits(w, h[s:s + lb])])
+            err = rowwise_rel_err(got[b], ref)
+            assert err < tol, f"seq {b} ({'bf16' if rnd else 'fp64'} oracle): logits rel err {err}"
+    model.close()
+
+
+# ---------------------------------------------------------------- one step, teacher forced
+def oracle_trajectory(prov, tokens0, prm):
+    """[(tokens before, block_start, block_steps, StepResult)] of a full decode."""
+    out = []
+    tok = np.asarray(tokens0, dtype=np.int64).copy()
+    for blk in range(prm.gen_len // prm.block_len):
+        bs, steps = blk * prm.block_len, 0
+        c0 = prm.prompt_len + bs
+        while True:
+            r = W.step(prov, tok, prm, bs, steps)
+            out.append((tok.copy(), bs, steps, r))
+            tok = r.tokens
+            steps += 1
+            if not np.any(tok[c0:c0 + prm.block_len] == prm.mask_id):
+                break
+    return out, tok
+
+
+@pytest.mark.parametrize("variant,tau1,tau2", [("wide", 0.7, 0.9), ("wide", 0.5, 0.9),
+                                               ("literal", 0.7, 0.9), ("wide", 0.95, 0.0)])
+def test_teacher_forced_steps(P, variant, tau1, tau2):
+    cfg, w = tiny(variant, seed=1)
+    wd = to_device(w)
+    p, g, lb = 32, 64, 16
+    model = P.WinoModel(cfg, wd, 2, p + g + lb)
+    prm_c = P.make_params(2, p, g, lb, cfg.mask_id, tau1, tau2)
+    prm = oracle_params(prm_c)
+    tok0 = batch_tokens(cfg, 2, p, g, seed=5)
+    trajs = [oracle_trajectory(W.ModelProvider(w, cfg), tok0[b], prm)[0] for b in range(2)]
+    n_cmp = 0
+    for k in range(max(len(t) for t in trajs)):
+        states = [t[min(k, len(t) - 1)] for t in trajs]
+        tokens = np.stack([s[0] for s in states])
+        gt, gf, gnm, gst, gstats = gpu_step(P, model, prm_c, tokens, [s[1] for s in states],
+                                            [s[2] for s in states])
+        for b, (tb, bs, steps, r) in enumerate(states):
+            c0 = p + bs
+            cur = tb[c0:c0 + lb]
+            n_cmp += compare_step(gt[b], gf[b], r, cur, cfg.mask_id, prm.tau1, c0, lb, f"step {k} seq {b}")
+            # nothing outside the current block may change
+            outside = np.ones(p + g, bool)
+            outside[c0:c0 + lb] = False
+            assert np.array_equal(gt[b][outside], tb[outside])
+            assert gst[b] == steps + 1
+            assert gnm[b] == np.sum(gt[b][c0:c0 + lb] == cfg.mask_id)
+            # the probability behind each decision, within bf16-pipeline accuracy
+            masked = cur == cfg.mask_id
+            val = np.exp(np.where(masked, gstats["z_best"][b], gstats["z_target"][b]) - gstats["m_all"][b]) / gstats["sumexp"][b]
+            ref = np.where(masked, r.conf, r.s)
+            assert np.max(np.abs(val - ref)) < 2e-2
+            assert np.array_equal(gstats["row_kind"][b], np.where(masked, 0, 1))
+    assert n_cmp > 0
+    model.close()
+
+
+# ---------------------------------------------------------------- free-running decode
+@pytest.mark.parametrize("variant,tau1,tau2,lb", [("wide", 0.7, 0.9, 16), ("literal", 0.7, 0.9, 16),
+                                                  ("wide", 0.6, 0.9, 64), ("wide", 0.8, 0.95, 8)])
+def test_decode_matches_oracle(P, variant, tau1, tau2, lb):
+    cfg, w = tiny(variant, seed=2)
+    wd = to_device(w)
+    p, g, B = 32, 64, 2
+    model = P.WinoModel(cfg, wd, B, p + g + lb)
+    prm_c = P.make_params(B, p, g, lb, cfg.mask_id, tau1, tau2)
+    prm = oracle_params(prm_c)
+    tok0 = batch_tokens(cfg, B, p, g, seed=9)
+    tok = torch.tensor(tok0, dtype=torch.int32, device="cuda")
+    bs = torch.zeros(B, dtype=torch.int32, device="cuda")
+    steps, forwards = P.wino_decode(model.ctx, prm_c, tok, bs)
+    torch.cuda.synchronize()
+    got = tok.cpu().numpy()
+    assert np.all(bs.cpu().numpy() == g)
+    assert not np.any(got[:, p:] == cfg.mask_id)
+    assert np.array_equal(got[:, :p], tok0[:, :p])
+    assert forwards == max(steps)
+    for b in range(B):
+        traj, final = oracle_trajectory(W.ModelProvider(w, cfg), tok0[b], prm)
+        robust = all(np.all(decided_mask(r.margin, r.top2_gap, t[c0:c0 + lb] == cfg.mask_id))
+                     and (not np.any(r.flags == W.FORCED)
+                          or forced_is_robust(r.conf, t[c0:c0 + lb] == cfg.mask_id))
+                     for (t, bs_, _, r) in traj for c0 in [p + bs_])
+        if robust:
+            assert np.array_equal(got[b], final), f"seq {b}: decoded tokens differ"
+            assert steps[b] == len(traj)
+    model.close()
+
+
+def test_decode_block_and_idle_sequences(P):
+    cfg, w = tiny("wide", seed=4)
+    wd = to_device(w)
+    p, g, lb, B = 16, 32, 16, 3
+    model = P.WinoModel(cfg, wd, B, p + g + lb)
+    prm_c = P.make_params(B, p, g, lb, cfg.mask_id, 0.7, 0.9)
+    tok0 = batch_tokens(cfg, B, p, g, seed=2)
+    tok0[1, p:p + lb] = 7              # sequence 1: current block already complete
+    tok = torch.tensor(tok0, dtype=torch.int32, device="cuda")
+    bs = torch.tensor([0, 0, g], dtype=torch.int32, device="cuda")  # sequence 2 finished
+    steps = P.wino_decode_block(model.ctx, prm_c, tok, bs)
+    torch.cuda.synchronize()
+    got = tok.cpu().numpy()
+    assert steps[1] == 0 and steps[2] == 0 and 1 <= steps[0] <= lb
+    assert np.array_equal(got[1], tok0[1]) and np.array_equal(got[2], tok0[2])
+    assert not np.any(got[0, p:p + lb] == cfg.mask_id)
+    assert np.array_equal(got[0, p + lb:], tok0[0, p + lb:])
+    model.close()
+
+
+def test_step_is_deterministic(P):
+    cfg, w = tiny("wide", seed=6)
+    wd = to_device(w)
+    p, g, lb, B = 32, 64, 16, 2
+    model = P.WinoModel(cfg, wd, B, p + g + lb)
+    prm_c = P.make_params(B, p, g, lb, cfg.mask_id)
+    tok0 = batch_tokens(cfg, B, p, g, seed=1, fill=[(0, 16, 0.5)])
+    a = gpu_step(P, model, prm_c, tok0, [0, 0], [1, 1])
+    b = gpu_step(P, model, prm_c, tok0, [0, 0], [1, 1])
+    for x, y in zip(a, b):
+        assert np.array_equal(x.view(np.uint8), y.view(np.uint8))
+    model.close()
+
+
+# ---------------------------------------------------------------- standalone epilogue
+@pytest.mark.parametrize("B,lb,V,heights", [(2, 8, 4096, (10.0, 16.0)), (8, 32, 126464, (10.0, 16.0)),
+                                            (8, 32, 126464, (0.0, 12.0)), (3, 5, 1000, (0.0, 14.0))])
+def test_epilogue_matches_oracle(P, B, lb, V, heights):
+    mask = V - 1 if V != 126464 else 126463
+    logits, cur, _ = wi.epilogue_inputs(B, lb, V, mask, seed=2, heights=heights, device="cuda")
+    cur0 = cur.cpu().numpy()
+    prm = P.make_params(B, 1, lb, lb, mask, 0.7, 0.9)
+    ws = torch.empty(P.wino_epilogue_workspace_bytes(B, lb, V), dtype=torch.uint8, device="cuda")
+    bitmap = torch.full((B, lb), 9, dtype=torch.uint8, device="cuda")
+    flags = torch.full((B, lb), 9, dtype=torch.uint8, device="cuda")
+    stats = torch.zeros(B * lb * STATS_DT.itemsize, dtype=torch.uint8, device="cuda")
+    P.wino_epilogue(prm, V, logits, cur, bitmap, flags, stats, ws)
+    torch.cuda.synchronize()
+    ref = E.decide(logits.cpu(), cur0, mask, float(np.float32(0.7)), float(np.float32(0.9)))
+    gt, gb, gf = cur.cpu().numpy(), bitmap.cpu().numpy(), flags.cpu().numpy()
+    st = stats.cpu().numpy().view(STATS_DT).reshape(B, lb)
+    z = logits.cpu().double().numpy()
+    for b in range(B):
+        masked = cur0[b] == mask
+        rows = np.where(masked, np.arange(lb), lb + np.arange(lb))
+        zr = z[b, rows]
+        # exact statistics: bf16 inputs are exact in fp32
+        assert np.array_equal(st["m_all"][b], zr.max(-1).astype(np.float32))
+        np.testing.assert_allclose(st["sumexp"][b], np.exp(zr - zr.max(-1, keepdims=True)).sum(-1), rtol=1e-5)
+        zx = zr.copy()
+        zx[:, mask] = -np.inf
+        assert np.array_equal(st["argmax"][b], zx.argmax(-1))
+        ok = decided_mask(ref["margin"][b], ref["gap"][b], masked)
+        if masked.any() and not np.any(ref["conf"][b][masked] > 0.7 + MARGIN):
+            ok &= ~masked
+        assert np.array_equal(gf[b][ok], ref["flags"][b][ok])
+        assert np.array_equal(gt[b][ok], ref["tokens"][b][ok])
+        assert np.array_equal(gb[b][ok], ref["bitmap"][b][ok])
+
+
+# ---------------------------------------------------------------- full-size shapes, one layer
+def big_one_layer(name, seed=0, wide=True):
+    cfg = wi.preset(name, n_layers=1)
+    lhs = wi.wide_lm_head_std(cfg) if wide else None
+    w = wi.model_weights(cfg, seed=seed, device="cuda", lm_head_std=lhs, gain_std=0.1)
+    return cfg, w
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name,B,p,g,lb,check,image", [("llada8b", 1, 256, 256, 32, [0], 0),
+                                                       ("llada8b", 16, 256, 256, 32, [0, 11], 0),
+                                                       ("mmada8b", 4, 1024, 1024, 64, [2], 576)])
+def test_full_shape_one_layer_step(P, name, B, p, g, lb, check, image):
+    cfg, wd = big_one_layer(name)
+    model = P.WinoModel(cfg, wd, B, p + g + lb)
+    tau1 = 0.6 if name == "mmada8b" else 0.7
+    prm_c = P.make_params(B, p, g, lb, cfg.mask_id, tau1, 0.9)
+    prm = oracle_params(prm_c)
+    pr = wi.prompts(cfg, B, p, seed=1, image_prefix=image).numpy()
+    tok0 = np.concatenate([pr, np.full((B, g), cfg.mask_id)], axis=1).astype(np.int64)
+    rng = np.random.default_rng(0)
+    bstart = [lb * (b % (g // lb)) for b in range(B)]
+    for b in range(B):   # earlier blocks decoded; current block partly drafted
+        tok0[b, p:p + bstart[b]] = rng.integers(0, cfg.mask_id, bstart[b])
+        c0 = p + bstart[b]
+        sel = np.arange(c0, c0 + lb)[rng.random(lb) < 0.5]
+        tok0[b, sel] = rng.integers(0, cfg.mask_id, len(sel))
+    gt, gf, gnm, gst, gstats = gpu_step(P, model, prm_c, tok0, bstart, [1] * B)
+    logits = torch.empty(B, 2 * lb, cfg.vocab, dtype=torch.float32, device="cuda")
+    P.wino_debug_logits(model.ctx, prm_c, torch.tensor(tok0, dtype=torch.int32, device="cuda"),
+                        torch.tensor(bstart, dtype=torch.int32, device="cuda"), logits)
+    torch.cuda.synchronize()
+    w = to_cpu(wd)
+    model.close()
+    del wd
+    for b in check:
+        prov = W.ModelProvider(w, cfg)
+        r = W.step(prov, tok0[b], prm, bstart[b], 1)
+        c0 = p + bstart[b]
+        err = rowwise_rel_err(logits[b].cpu().numpy(), np.concatenate([r.z_cur, r.z_shad]))
+        assert err < LOGIT_TOL, f"seq {b}: logits rel err {err}"
+        n = compare_step(gt[b], gf[b], r, tok0[b][c0:c0 + lb], cfg.mask_id, prm.tau1, c0, lb, f"seq {b}")
+        assert n > 0
