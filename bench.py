@@ -1,0 +1,226 @@
+"""Benchmark of one WINO decoding step at the LLaDA-8B shape on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config bs16|bs1|mmada|tiny]
+
+A "step" is one pass of the whole hot path through the C ABI (wino_step):
+embedding, 32 layers of bidirectional attention with the shadow block and
+SwiGLU FFN, the final norm of the rows the decision reads, the LM head with its
+fused softmax statistics and the draft / verify update, for every sequence of
+the batch.  Inputs (random-init bf16 weights of the 8B architecture, seeded
+prompts) are resident in HBM before timing starts; each timed step starts from
+the same mid-block decoding state (a 32 KB device copy restores it).
+
+One JSON line is printed.  `value` is steps/s; the line also carries
+generated tokens/s from a full semi-autoregressive decode, the dominant
+kernel's roofline figures measured with HIP events during the timed region,
+and the CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "WINO denoise steps/s + gen tokens/s, LLaDA-8B shape bs1/bs16; MFMA util %"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+CONFIGS = {
+    # name: (preset, batch, prompt, gen, block, tau1, tau2, image_prefix)
+    "bs16": ("llada8b", 16, 256, 256, 32, 0.7, 0.9, 0),
+    "bs1": ("llada8b", 1, 256, 256, 32, 0.7, 0.9, 0),
+    "mmada": ("mmada8b", 4, 1024, 1024, 64, 0.6, 0.9, 576),
+    "tiny": ("tiny", 1, 32, 64, 16, 0.7, 0.9, 0),
+}
+DOMINANT = "gemm_gateup_swiglu"
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def make_state(wi, cfg, B, p, g, lb, image_prefix, seed=1000):
+    """Prompt ids, then a decoded first block and a half-drafted second block."""
+    import torch
+    pr = wi.prompts(cfg, B, p, seed=seed, image_prefix=image_prefix)
+    tok = wi.initial_tokens(pr, g, cfg.mask_id)
+    u = wi.uniform(seed, 77, B * g).view(B, g)
+    rnd = wi.randint(seed, 78, B * g, 0, cfg.mask_id).view(B, g).to(torch.int32)
+    gen = tok[:, p:]
+    filled = torch.zeros(B, g, dtype=torch.bool)
+    filled[:, :lb] = True
+    filled[:, lb:2 * lb] = u[:, lb:2 * lb] < 0.5
+    gen[filled] = rnd[filled]
+    block_start = torch.full((B,), lb, dtype=torch.int32)
+    return tok.contiguous(), block_start
+
+
+def run_workload(P, wi, cfg, weights, name, steps, warmup, profile_dominant=True):
+    import torch
+    preset, B, p, g, lb, tau1, tau2, img = CONFIGS[name]
+    model = P.WinoModel(cfg, weights, B, p + g + lb)
+    prm = P.make_params(B, p, g, lb, cfg.mask_id, tau1, tau2)
+    tok0, bs0 = make_state(wi, cfg, B, p, g, lb, img)
+    tok0, bs0 = tok0.cuda(), bs0.cuda()
+    tok = tok0.clone()
+    bs = bs0.clone()
+    st0 = torch.ones(B, dtype=torch.int32, device="cuda")
+    st = st0.clone()
+    flags = torch.empty(B, lb, dtype=torch.uint8, device="cuda")
+    nm = torch.empty(B, dtype=torch.int32, device="cuda")
+
+    def one_step():
+        tok.copy_(tok0)
+        st.copy_(st0)
+        P.wino_step(model.ctx, prm, tok, bs, st, flags, nm)
+
+    for _ in range(warmup):
+        one_step()
+    torch.cuda.synchronize()
+    classes = {P.wino_kernel_class_name(i): i for i in range(12)}
+    if profile_dominant:
+        P.wino_profile(model.ctx, 1 << classes[DOMINANT])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        one_step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    dom = P.wino_profile_read(model.ctx)[DOMINANT] if profile_dominant else None
+    P.wino_profile(model.ctx, 0)
+
+    # per-kernel breakdown (separate pass, not part of the timed value)
+    P.wino_profile(model.ctx, (1 << 12) - 1)
+    for _ in range(2):
+        one_step()
+    torch.cuda.synchronize()
+    per = P.wino_profile_read(model.ctx)
+    P.wino_profile(model.ctx, 0)
+    kernels = {}
+    for k, v in per.items():
+        if v["launches"] == 0:
+            continue
+        ms = v["ms"] / 2
+        kernels[k] = {"ms_per_step": round(ms, 4), "launches_per_step": v["launches"] // 2,
+                      "tflops": round(v["flops"] / 2 / (ms * 1e-3) / 1e12, 2) if v["flops"] else None,
+                      "gbs": round(v["bytes"] / 2 / (ms * 1e-3) / 1e9, 1) if v["bytes"] else None}
+
+    # full decode from the prompt: generated tokens per second
+    pr_tok = wi.initial_tokens(wi.prompts(cfg, B, p, seed=1000, image_prefix=img), g, cfg.mask_id).cuda()
+    dbs = torch.zeros(B, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    seq_steps, forwards = P.wino_decode(model.ctx, prm, pr_tok, dbs)
+    torch.cuda.synchronize()
+    dec_s = time.perf_counter() - t1
+    model.close()
+    return {"elapsed": elapsed, "dominant": dom, "kernels": kernels,
+            "decode": {"forwards": forwards, "seconds": round(dec_s, 4),
+                       "tokens_per_s": round(B * g / dec_s, 2),
+                       "steps_per_seq_mean": sum(seq_steps) / len(seq_steps)}}
+
+
+def cpu_baseline(wi, cfg, weights, name):
+    """The float64 oracle on a bounded sample: one layer of one sequence plus
+    the LM head of its block rows, extrapolated to a full batched step."""
+    import numpy as np
+    import torch
+    from oracle import model as M
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count()])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count()
+    preset, B, p, g, lb, tau1, tau2, img = CONFIGS[name]
+    lw = {k: v.cpu() for k, v in weights["layers"][0].items()}
+    tok, bs = make_state(wi, cfg, 1, p, g, lb, img)
+    ext, pos, allowed, c0 = M.extended_inputs(tok[0].numpy(), p, g, lb, int(bs[0]), cfg.mask_id)
+    emb_rows = weights["tok_emb"][torch.as_tensor(ext).cuda()].cpu()
+    w1 = {"tok_emb": emb_rows, "layers": [lw], "final_norm": weights["final_norm"].cpu(),
+          "lm_head": weights["lm_head"].cpu(), "lm_bias": weights["lm_bias"].cpu()}
+    t0 = time.perf_counter()
+    x = M.forward_residual(w1, cfg, np.arange(len(ext)), pos, allowed, n_layers=1)
+    t_layer = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    h = M.rmsnorm(x[c0:c0 + lb], M.f64(w1["final_norm"]), cfg.rms_eps)
+    M.lm_logits(w1, h)
+    t_head = time.perf_counter() - t0
+    per_seq = cfg.n_layers * t_layer + t_head
+    step_s = B * per_seq
+    return {"value": round(1.0 / step_s, 6), "unit": "steps/s", "cores": int(cores), "kind": "oracle",
+            "seconds_per_step": round(step_s, 2),
+            "sample": (f"float64 numpy oracle: 1 of {cfg.n_layers} layers for 1 of {B} sequences "
+                       f"(T={len(ext)}) took {t_layer:.2f}s, LM head for its {lb} block rows "
+                       f"{t_head:.2f}s; extrapolated x{cfg.n_layers} layers x{B} sequences")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="bs16", choices=sorted(CONFIGS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-bs1", action="store_true")
+    a = ap.parse_args()
+    if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the WINO step is benchmarked on a single MI355X "
+              "(multi-GPU sharding is a design note, not part of this build).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2605_16941_amd as P
+    import wino_inputs as wi
+
+    preset = CONFIGS[a.config][0]
+    cfg = wi.preset(preset)
+    log(f"generating {preset} weights on the GPU")
+    t0 = time.perf_counter()
+    weights = wi.model_weights(cfg, seed=0, device="cuda")
+    torch.cuda.synchronize()
+    log(f"weights ready in {time.perf_counter() - t0:.1f}s")
+
+    res = run_workload(P, wi, cfg, weights, a.config, a.steps, a.warmup)
+    _, B, p, g, lb, tau1, tau2, img = CONFIGS[a.config]
+    ms = res["elapsed"] / a.steps * 1e3
+    dom = res["dominant"]
+    dom_ms = dom["ms"] / max(dom["launches"], 1)
+    dom_flops = dom["flops"] / max(dom["launches"], 1)
+    achieved = dom_flops / (dom_ms * 1e-3) / 1e12
+    line = {
+        "metric": METRIC, "value": round(1e3 / ms, 4), "unit": "steps/s", "n_gpus": 1,
+        "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded random-init weights of the architecture, seeded prompts)",
+        "config": {"workload": f"{preset} WINO step, batch {B}, prompt {p}, gen {g}, block {lb}",
+                   "batch": B, "prompt_len": p, "gen_len": g, "block_len": lb, "tau1": tau1,
+                   "tau2": tau2, "init": "literal (LM head std 0.5/sqrt(d), Zipf bias)"},
+        "tokens_per_s": res["decode"]["tokens_per_s"],
+        "decode": res["decode"],
+        "roofline": {"bound": "mfma", "kernel": DOMINANT, "achieved": round(achieved, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None, "avg_launch_ms": round(dom_ms, 4),
+                     "flops_per_launch": dom_flops, "launches": dom["launches"]},
+        "kernels": res["kernels"],
+    }
+    if a.config == "bs16" and not a.no_bs1:
+        log("bs1 workload")
+        r1 = run_workload(P, wi, cfg, weights, "bs1", a.steps, a.warmup)
+        ms1 = r1["elapsed"] / a.steps * 1e3
+        line["bs1"] = {"steps_per_s": round(1e3 / ms1, 3), "ms_per_step": round(ms1, 3),
+                       "tokens_per_s": r1["decode"]["tokens_per_s"], "decode": r1["decode"],
+                       "kernels": r1["kernels"]}
+    if not a.no_cpu_baseline:
+        log("cpu baseline (oracle sample)")
+        line["cpu_baseline"] = cpu_baseline(wi, cfg, weights, a.config)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -170,11 +170,13 @@ wino_status wino_epilogue(const wino_params* p, int32_t vocab, const void* d_log
  * wino_debug_logits: fp32 logits [batch, 2*block_len, vocab] of the current
  *   block rows (0..Lb-1) and shadow rows (Lb..2Lb-1) for the given state.
  * wino_debug_forward: residual stream fp32 [batch, T, d] (T = prompt_len +
- *   gen_len + block_len) after the embedding and the first n_layers layers. */
+ *   gen_len + block_len) after the embedding and the first n_sublayers
+ *   sublayers; each layer is two sublayers, attention then FFN, so
+ *   n_sublayers = 2*n_layers is the full backbone before the final norm. */
 wino_status wino_debug_logits(wino_ctx* ctx, const wino_params* p, const int32_t* d_tokens,
                               const int32_t* d_block_start, float* d_logits, void* stream);
 wino_status wino_debug_forward(wino_ctx* ctx, const wino_params* p, const int32_t* d_tokens,
-                               const int32_t* d_block_start, int32_t n_layers, float* d_out,
+                               const int32_t* d_block_start, int32_t n_sublayers, float* d_out,
                                void* stream);
 
 /* Kernel timing with HIP events on the launch stream.  enable != 0 records a

@@ -18,9 +18,11 @@ What WINO itself changes in the forward (Sec. 4.2.2):
   including itself - the paper excludes only the corresponding Y_cur position).
 
 Optional ``act_round`` rounds activations at the points where a bf16 pipeline
-materialises them (normed inputs of each matrix product, q/k/v after RoPE, the
-attention output, the SwiGLU product).  With ``act_round=None`` everything stays
-in float64.
+materialises them: the normed inputs of the backbone's matrix products, q/k/v
+after RoPE, the attention output and the SwiGLU product.  The final normed
+hidden state feeding the LM head is not rounded (a pipeline that keeps it as a
+hi+lo pair of bf16 values carries 16 mantissa bits there).  With
+``act_round=None`` everything stays in float64.
 """
 from __future__ import annotations
 
@@ -108,11 +110,11 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, allowed: np.ndarray) 
     return np.matmul(p, vh).transpose(1, 0, 2)
 
 
-def layer_forward(x: np.ndarray, lw: dict, cfg, cos, sin, allowed, act_round=None) -> np.ndarray:
-    """One transformer layer on the residual stream x [T, d] (float64)."""
+def attention_sublayer(x: np.ndarray, lw: dict, cfg, cos, sin, allowed, act_round=None) -> np.ndarray:
+    """x + Attn(RMSNorm(x)) W_o^T on the residual stream x [T, d] (float64)."""
     rnd = act_round or (lambda a: a)
     t, d = x.shape
-    nh, hd, ff = cfg.n_heads, cfg.head_dim, cfg.d_ff
+    nh, hd = cfg.n_heads, cfg.head_dim
     h = rnd(rmsnorm(x, f64(lw["attn_norm"]), cfg.rms_eps))
     qkv = h @ f64(lw["w_qkv"]).T
     q = qkv[:, :d].reshape(t, nh, hd)
@@ -122,31 +124,48 @@ def layer_forward(x: np.ndarray, lw: dict, cfg, cos, sin, allowed, act_round=Non
     k = rnd(apply_rope(k, cos, sin))
     v = rnd(v)
     o = rnd(attention(q, k, v, allowed).reshape(t, d))
-    x = x + o @ f64(lw["w_o"]).T
+    return x + o @ f64(lw["w_o"]).T
+
+
+def ffn_sublayer(x: np.ndarray, lw: dict, cfg, act_round=None) -> np.ndarray:
+    """x + (SiLU(h W_g^T) * h W_u^T) W_d^T with h = RMSNorm(x)."""
+    rnd = act_round or (lambda a: a)
+    ff = cfg.d_ff
     h = rnd(rmsnorm(x, f64(lw["ffn_norm"]), cfg.rms_eps))
     gu = h @ f64(lw["w_gate_up"]).T
     a = rnd(silu(gu[:, :ff]) * gu[:, ff:])
     return x + a @ f64(lw["w_down"]).T
 
 
+def layer_forward(x: np.ndarray, lw: dict, cfg, cos, sin, allowed, act_round=None) -> np.ndarray:
+    """One transformer layer: attention sublayer then FFN sublayer."""
+    x = attention_sublayer(x, lw, cfg, cos, sin, allowed, act_round)
+    return ffn_sublayer(x, lw, cfg, act_round)
+
+
 def forward_residual(weights: dict, cfg, tokens, pos, allowed, act_round=None,
-                     n_layers: int | None = None) -> np.ndarray:
-    """Residual stream [T, d] after the embedding and the first n_layers layers."""
+                     n_layers: int | None = None, n_sublayers: int | None = None) -> np.ndarray:
+    """Residual stream [T, d] after the embedding and the first n_layers layers
+    (or the first n_sublayers sublayers: attention and FFN of each layer)."""
     tokens = np.asarray(tokens, dtype=np.int64)
     x = f64(weights["tok_emb"][torch.as_tensor(tokens)])
     cos, sin = rope_cos_sin(pos, cfg.head_dim, cfg.rope_theta)
-    nl = cfg.n_layers if n_layers is None else n_layers
-    for layer in range(nl):
-        x = layer_forward(x, weights["layers"][layer], cfg, cos, sin, allowed, act_round)
+    if n_sublayers is None:
+        n_sublayers = 2 * (cfg.n_layers if n_layers is None else n_layers)
+    for i in range(n_sublayers):
+        lw = weights["layers"][i // 2]
+        if i % 2 == 0:
+            x = attention_sublayer(x, lw, cfg, cos, sin, allowed, act_round)
+        else:
+            x = ffn_sublayer(x, lw, cfg, act_round)
     return x
 
 
 def forward_hidden(weights: dict, cfg, tokens, pos, allowed, act_round=None,
                    n_layers: int | None = None) -> np.ndarray:
     """Final-normed hidden states [T, d] for token ids ``tokens`` [T]."""
-    rnd = act_round or (lambda a: a)
     x = forward_residual(weights, cfg, tokens, pos, allowed, act_round, n_layers)
-    return rnd(rmsnorm(x, f64(weights["final_norm"]), cfg.rms_eps))
+    return rmsnorm(x, f64(weights["final_norm"]), cfg.rms_eps)
 
 
 def lm_logits(weights: dict, h_rows: np.ndarray) -> np.ndarray:

@@ -209,10 +209,10 @@ def wino_debug_logits(ctx, p: wino_params, tokens, block_start, logits, stream=N
            "wino_debug_logits", ctx)
 
 
-def wino_debug_forward(ctx, p: wino_params, tokens, block_start, n_layers, out, stream=None) -> None:
+def wino_debug_forward(ctx, p: wino_params, tokens, block_start, n_sublayers, out, stream=None) -> None:
     import torch
     _check(lib.wino_debug_forward(ctx, C.byref(p), _ptr(tokens, torch.int32, "tokens"),
-                                  _ptr(block_start, torch.int32, "block_start"), n_layers,
+                                  _ptr(block_start, torch.int32, "block_start"), n_sublayers,
                                   _ptr(out, torch.float32, "out"), _stream(stream)),
            "wino_debug_forward", ctx)
 

@@ -11,9 +11,9 @@
 // Each wave owns 32 query rows.  Scores are computed transposed, S^T = K Q^T,
 // so after the 32x32x16 MFMA a lane holds 32 keys of ONE query row: the
 // online-softmax max / sum stay inside the lane (plus its partner lane 32
-// apart).  The same registers, rounded to bf16, are the B operand of
-// O^T = V^T P^T, whose A operand comes from the transposed V tile in LDS;
-// the per-lane key order of P and V^T is matched slot by slot.
+// apart).  The same registers, split into hi and lo bf16 parts, are the B
+// operand of O^T = V^T P^T, whose A operand comes from the transposed V tile
+// in LDS; the per-lane key order of P and V^T is matched slot by slot.
 #include "common.h"
 #include "kernels.h"
 
@@ -129,20 +129,26 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(StepGeom g, const uint16_
 
 #pragma unroll
     for (int ks4 = 0; ks4 < BKV / 16; ++ks4) {
+      // P as hi + lo bf16 parts: the product with V keeps ~16 mantissa bits
+      // of the probabilities instead of bf16's 8
       const int base = 8 * (ks4 & 1);
-      uint4 praw;
-      praw.x = pack2bf(s[ks4 >> 1][base + 0], s[ks4 >> 1][base + 1]);
-      praw.y = pack2bf(s[ks4 >> 1][base + 2], s[ks4 >> 1][base + 3]);
-      praw.z = pack2bf(s[ks4 >> 1][base + 4], s[ks4 >> 1][base + 5]);
-      praw.w = pack2bf(s[ks4 >> 1][base + 6], s[ks4 >> 1][base + 7]);
-      const bf16x8 pf = as_bf16x8(praw);
+      uint32_t ph[4], pl[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float p0 = s[ks4 >> 1][base + 2 * e], p1 = s[ks4 >> 1][base + 2 * e + 1];
+        ph[e] = pack2bf(p0, p1);
+        pl[e] = pack2bf(p0 - bf2f((uint16_t)(ph[e] & 0xFFFFu)), p1 - bf2f((uint16_t)(ph[e] >> 16)));
+      }
+      const bf16x8 pf_hi = as_bf16x8(make_uint4(ph[0], ph[1], ph[2], ph[3]));
+      const bf16x8 pf_lo = as_bf16x8(make_uint4(pl[0], pl[1], pl[2], pl[3]));
 #pragma unroll
       for (int fe = 0; fe < FE; ++fe) {
         const uint16_t* vr = Vs + (fe * 32 + (lane & 31)) * LDV + 16 * ks4 + 4 * grp;
         const uint2 lo = *reinterpret_cast<const uint2*>(vr);
         const uint2 hi = *reinterpret_cast<const uint2*>(vr + 8);
         const bf16x8 vf = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
-        oacc[fe] = mfma32(vf, pf, oacc[fe]);
+        oacc[fe] = mfma32(vf, pf_hi, oacc[fe]);
+        oacc[fe] = mfma32(vf, pf_lo, oacc[fe]);
       }
     }
   }

@@ -7,11 +7,16 @@
 //   logit of the current token) so the logits never reach memory,
 //   plain fp32 store (+bias) for the test entry point.
 //
+// The LM-head epilogues read the final hidden rows as two bf16 parts (hi and
+// lo of the fp32 value) and multiply both with the same W tile, so the logits
+// carry ~16 mantissa bits of the hidden state instead of bf16's 8.
+//
 // Tiling: a workgroup owns a BM x BN output tile and walks K in steps of 64.
-// A and W tiles are staged global -> registers -> LDS (rows padded by 16 bytes
-// so that the 16-byte fragment reads of 8 consecutive rows hit distinct bank
-// groups); the next K step is fetched into registers while the matrix cores
-// consume the current one.  Waves form a WM x WN grid, each owning a
+// A and W tiles go straight from global memory into LDS (gfx950 LDS-DMA,
+// global_load_lds_dwordx4: no staging registers), double-buffered so the next
+// K step streams in while the matrix cores consume the current one.  Within a
+// tile row the 16-byte chunks are XOR-swizzled by the row index, so the
+// fragment reads of 8 consecutive rows hit distinct bank groups.  Waves form a WM x WN grid, each owning a
 // (BM/WM) x (BN/WN) sub-tile of 32x32 MFMA blocks.  Workgroups are renumbered
 // so that each XCD works on one contiguous range of tiles (shared W tiles stay
 // in that XCD's L2).
@@ -213,45 +218,70 @@ __device__ __forceinline__ void epi_lmstats(const GemmCall& c, f32x16 (&acc)[FM]
 
 template <int BM, int BN, int WM, int WN, int EPI>
 __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
-  constexpr int NT = WM * WN * 64;
+  constexpr int NW = WM * WN;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int FM = WTM / 32, FN = WTN / 32;
-  constexpr int AC = BM * BK / 8 / NT;
-  constexpr int BC = BN * BK / 8 / NT;
-  static_assert(AC >= 1 && BC >= 1 && AC * NT * 8 == BM * BK && BC * NT * 8 == BN * BK,
-                "tile / thread split");
+  // LM-head epilogues multiply W with both bf16 parts (hi, lo) of the fp32 rows
+  constexpr bool SPLIT = EPI == EPI_LMSTATS || EPI == EPI_STORE_F32;
+  constexpr int AROWS = SPLIT ? 2 * BM : BM;
+  // one LDS-DMA instruction moves 64 lanes x 16 bytes = 8 tile rows of 64 bf16
+  constexpr int A_INS = AROWS / (8 * NW);
+  constexpr int B_INS = BN / (8 * NW);
+  static_assert(A_INS * 8 * NW == AROWS && B_INS * 8 * NW == BN, "loader split");
   static_assert(FM >= 1 && FN >= 1, "wave tile");
+  constexpr int STAGE = (AROWS + BN) * BK;  // bf16 elements per pipeline stage
 
-  __shared__ __attribute__((aligned(16))) uint16_t smem[(BM + BN) * LDK];
-  uint16_t* As = smem;
-  uint16_t* Bs = smem + BM * LDK;
+  __shared__ __attribute__((aligned(1024))) uint16_t smem[2 * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave - (wave / WN) * WN;
-  const int nTM = (c.M + BM - 1) / BM;
-  const int tile = xcd_remap(blockIdx.x, gridDim.x);
-  const int tm = tile % nTM, tn = tile / nTM;
+  // Tile order: each XCD takes a contiguous range of logical tiles, walked in
+  // groups of GM M-tiles so the ~32 workgroups an XCD runs at once cover
+  // GM A tiles x (32/GM) W tiles and reuse both from its L2.
+  constexpr int GM = 8;
+  const int nTM = (c.M + BM - 1) / BM, nTN = c.N / BN;
+  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  const int first_m = (t / (GM * nTN)) * GM;
+  const int gsz = min(nTM - first_m, GM);
+  const int tm = first_m + (t % (GM * nTN)) % gsz;
+  const int tn = (t % (GM * nTN)) / gsz;
   const int m0 = tm * BM, n0 = tn * BN;
 
-  const uint16_t* ap[AC];
-  int al[AC];
+  // Tile rows are 128 bytes = 8 chunks of 16 bytes; chunk kc of row r is
+  // stored at position kc ^ (r & 7).  The lane that fills position (lane & 7)
+  // of row (8*i + lane/8) therefore fetches chunk (lane & 7) ^ (lane >> 3).
+  const int lrow = lane >> 3;
+  const int lkc = (lane & 7) ^ lrow;
+  const uint16_t* asrc[A_INS];
 #pragma unroll
-  for (int j = 0; j < AC; ++j) {
-    const int q = tid + j * NT, r = q >> 3, kc = q & 7;
-    const int gm = min(m0 + r, c.M - 1);
-    ap[j] = c.A + (size_t)gm * c.lda + kc * 8;
-    al[j] = r * LDK + kc * 8;
+  for (int i = 0; i < A_INS; ++i) {
+    const int row = (wave * A_INS + i) * 8 + lrow;
+    const bool lo = SPLIT && row >= BM;
+    const int gm = min(m0 + (lo ? row - BM : row), c.M - 1);
+    asrc[i] = (lo ? c.A2 : c.A) + (size_t)gm * c.lda + lkc * 8;
   }
-  const uint16_t* bp[BC];
-  int bl[BC];
+  const uint16_t* bsrc[B_INS];
 #pragma unroll
-  for (int j = 0; j < BC; ++j) {
-    const int q = tid + j * NT, r = q >> 3, kc = q & 7;
-    const int vc = n0 + r;
+  for (int i = 0; i < B_INS; ++i) {
+    const int vc = n0 + (wave * B_INS + i) * 8 + lrow;
     const int wr = EPI == EPI_SWIGLU ? swiglu_row<WTN>(vc, c.F) : vc;
-    bp[j] = c.W + (size_t)wr * c.ldw + kc * 8;
-    bl[j] = r * LDK + kc * 8;
+    bsrc[i] = c.W + (size_t)wr * c.ldw + lkc * 8;
   }
+
+  auto issue = [&](int kt, int stage) {
+    uint16_t* sA = smem + stage * STAGE;
+    uint16_t* sB = sA + AROWS * BK;
+#pragma unroll
+    for (int i = 0; i < A_INS; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + kt * BK),
+                                       (__attribute__((address_space(3))) void*)(sA + (wave * A_INS + i) * 512),
+                                       16, 0, 0);
+#pragma unroll
+    for (int i = 0; i < B_INS; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(bsrc[i] + kt * BK),
+                                       (__attribute__((address_space(3))) void*)(sB + (wave * B_INS + i) * 512),
+                                       16, 0, 0);
+  };
 
   f32x16 acc[FM][FN];
 #pragma unroll
@@ -261,49 +291,43 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[fm][fn][i] = 0.f;
 
-  uint4 ra[AC], rb[BC];
-#pragma unroll
-  for (int j = 0; j < AC; ++j) ra[j] = *reinterpret_cast<const uint4*>(ap[j]);
-#pragma unroll
-  for (int j = 0; j < BC; ++j) rb[j] = *reinterpret_cast<const uint4*>(bp[j]);
-#pragma unroll
-  for (int j = 0; j < AC; ++j) *reinterpret_cast<uint4*>(As + al[j]) = ra[j];
-#pragma unroll
-  for (int j = 0; j < BC; ++j) *reinterpret_cast<uint4*>(Bs + bl[j]) = rb[j];
-  __syncthreads();
-
   const int nk = c.K / BK;
+  const int swz = lane & 7;  // == row & 7 for every fragment row this lane reads
   const int arow = wm * WTM + (lane & 31), brow = wn * WTN + (lane & 31);
+  issue(0, 0);
   for (int kt = 0; kt < nk; ++kt) {
-    const bool more = kt + 1 < nk;
-    if (more) {
-      const int ko = (kt + 1) * BK;
-#pragma unroll
-      for (int j = 0; j < AC; ++j) ra[j] = *reinterpret_cast<const uint4*>(ap[j] + ko);
-#pragma unroll
-      for (int j = 0; j < BC; ++j) rb[j] = *reinterpret_cast<const uint4*>(bp[j] + ko);
+    if (kt + 1 < nk) {
+      issue(kt + 1, (kt + 1) & 1);
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(A_INS + B_INS) : "memory");
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     }
+    __syncthreads();
+    const uint16_t* sA = smem + (kt & 1) * STAGE;
+    const uint16_t* sB = sA + AROWS * BK;
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
-      const int koff = ks * 16 + (lane >> 5) * 8;
+      const int kc = ((ks * 2 + (lane >> 5)) ^ swz) * 8;
       bf16x8 af[FM], bf[FN];
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
-        af[fm] = as_bf16x8(*reinterpret_cast<const uint4*>(As + (arow + fm * 32) * LDK + koff));
+        af[fm] = as_bf16x8(*reinterpret_cast<const uint4*>(sA + (arow + fm * 32) * BK + kc));
 #pragma unroll
       for (int fn = 0; fn < FN; ++fn)
-        bf[fn] = as_bf16x8(*reinterpret_cast<const uint4*>(Bs + (brow + fn * 32) * LDK + koff));
+        bf[fn] = as_bf16x8(*reinterpret_cast<const uint4*>(sB + (brow + fn * 32) * BK + kc));
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
         for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma32(af[fm], bf[fn], acc[fm][fn]);
-    }
-    __syncthreads();
-    if (more) {
+      if constexpr (SPLIT) {
 #pragma unroll
-      for (int j = 0; j < AC; ++j) *reinterpret_cast<uint4*>(As + al[j]) = ra[j];
+        for (int fm = 0; fm < FM; ++fm)
+          af[fm] = as_bf16x8(*reinterpret_cast<const uint4*>(sA + (BM + arow + fm * 32) * BK + kc));
 #pragma unroll
-      for (int j = 0; j < BC; ++j) *reinterpret_cast<uint4*>(Bs + bl[j]) = rb[j];
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma32(af[fm], bf[fn], acc[fm][fn]);
+      }
     }
     __syncthreads();
   }
@@ -324,29 +348,27 @@ struct TileCfg {
 
 constexpr TileCfg kTiles[] = {
     {256, 256, 2, 2, 1, 1.00f},
+    {192, 256, 2, 2, 1, 0.97f},
     {128, 256, 2, 2, 1, 0.90f},
     {128, 128, 2, 2, 2, 0.80f},
-    {64, 128, 2, 2, 4, 0.60f},
-    {32, 256, 1, 4, 3, 0.50f},
+    {64, 128, 2, 2, 3, 0.60f},
+    {32, 256, 1, 4, 2, 0.50f},
 };
 
 bool tile_ok(const GemmCall& c, const TileCfg& t) {
   if (c.N % t.BN || c.K % BK) return false;
   const int WTN = t.BN / t.WN;
+  const bool lm = c.epi == EPI_LMSTATS || c.epi == EPI_STORE_F32;
+  if (lm) return t.BM == 32 || (t.BM == 128 && t.BN == 256);
+  if (t.BM == 32) return false;
   switch (c.epi) {
     case EPI_QKV_ROPE:
-      // the 256x256 tile spills registers in this epilogue
-      return WTN == c.rope.hd && (c.rope.H * c.rope.hd) % t.BN == 0 && t.BM != 32 &&
-             t.BM != 256;
+      return t.BM != 256 && t.BM != 192 && WTN == c.rope.hd && (c.rope.H * c.rope.hd) % t.BN == 0;
     case EPI_SWIGLU:
-      return (c.F % (WTN / 2)) == 0 && t.BM != 32;
-    case EPI_RESIDUAL:
-      return t.BM != 32;
-    case EPI_LMSTATS:
-    case EPI_STORE_F32:
-      return t.BM == 32 || t.BM == 128 || t.BM == 256;
+      return (c.F % (WTN / 2)) == 0;
+    default:
+      return true;
   }
-  return false;
 }
 
 int pick_tile(const GemmCall& c) {
@@ -365,18 +387,38 @@ int pick_tile(const GemmCall& c) {
   return best;
 }
 
+// (tile, epilogue) pairs that are built: the LM-head epilogues double the A
+// tile (hi and lo parts), which only fits LDS for BM <= 128, and the RoPE
+// epilogue needs a wave to own a whole head and spills at 256x256.
+template <int BM, int BN, int EPI>
+constexpr bool built() {
+  if (EPI == EPI_LMSTATS || EPI == EPI_STORE_F32) return BM == 32 || (BM == 128 && BN == 256);
+  if (BM == 32) return false;
+  if (EPI == EPI_QKV_ROPE) return BM != 256 && BM != 192;
+  return true;
+}
+
+template <int BM, int BN, int WM, int WN, int EPI>
+hipError_t launch_one(const GemmCall& c, hipStream_t st) {
+  if constexpr (built<BM, BN, EPI>()) {
+    const int tiles = ((c.M + BM - 1) / BM) * (c.N / BN);
+    gemm_kernel<BM, BN, WM, WN, EPI><<<dim3(tiles), dim3(WM * WN * 64), 0, st>>>(c);
+    return hipGetLastError();
+  } else {
+    return hipErrorInvalidValue;
+  }
+}
+
 template <int BM, int BN, int WM, int WN>
 hipError_t launch_cfg(const GemmCall& c, hipStream_t st) {
-  const int tiles = ((c.M + BM - 1) / BM) * (c.N / BN);
-  dim3 grid(tiles), block(WM * WN * 64);
   switch (c.epi) {
-    case EPI_QKV_ROPE: gemm_kernel<BM, BN, WM, WN, EPI_QKV_ROPE><<<grid, block, 0, st>>>(c); break;
-    case EPI_RESIDUAL: gemm_kernel<BM, BN, WM, WN, EPI_RESIDUAL><<<grid, block, 0, st>>>(c); break;
-    case EPI_SWIGLU: gemm_kernel<BM, BN, WM, WN, EPI_SWIGLU><<<grid, block, 0, st>>>(c); break;
-    case EPI_LMSTATS: gemm_kernel<BM, BN, WM, WN, EPI_LMSTATS><<<grid, block, 0, st>>>(c); break;
-    case EPI_STORE_F32: gemm_kernel<BM, BN, WM, WN, EPI_STORE_F32><<<grid, block, 0, st>>>(c); break;
+    case EPI_QKV_ROPE: return launch_one<BM, BN, WM, WN, EPI_QKV_ROPE>(c, st);
+    case EPI_RESIDUAL: return launch_one<BM, BN, WM, WN, EPI_RESIDUAL>(c, st);
+    case EPI_SWIGLU: return launch_one<BM, BN, WM, WN, EPI_SWIGLU>(c, st);
+    case EPI_LMSTATS: return launch_one<BM, BN, WM, WN, EPI_LMSTATS>(c, st);
+    case EPI_STORE_F32: return launch_one<BM, BN, WM, WN, EPI_STORE_F32>(c, st);
   }
-  return hipGetLastError();
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
@@ -392,10 +434,11 @@ hipError_t launch_gemm(const GemmCall& c, hipStream_t st) {
   if (c.M <= 0) return hipSuccess;
   switch (i) {
     case 0: return launch_cfg<256, 256, 2, 2>(c, st);
-    case 1: return launch_cfg<128, 256, 2, 2>(c, st);
-    case 2: return launch_cfg<128, 128, 2, 2>(c, st);
-    case 3: return launch_cfg<64, 128, 2, 2>(c, st);
-    case 4: return launch_cfg<32, 256, 1, 4>(c, st);
+    case 1: return launch_cfg<192, 256, 2, 2>(c, st);
+    case 2: return launch_cfg<128, 256, 2, 2>(c, st);
+    case 3: return launch_cfg<128, 128, 2, 2>(c, st);
+    case 4: return launch_cfg<64, 128, 2, 2>(c, st);
+    case 5: return launch_cfg<32, 256, 1, 4>(c, st);
   }
   return hipErrorInvalidValue;
 }

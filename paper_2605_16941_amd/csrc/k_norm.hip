@@ -10,7 +10,8 @@ namespace {
 
 template <int CPL>
 __device__ __forceinline__ void norm_store(float (&v)[CPL][8], float ss, const uint16_t* gain,
-                                           float eps, int d, int lane, uint16_t* out) {
+                                           float eps, int d, int lane, uint16_t* out,
+                                           uint16_t* out_lo = nullptr) {
   const int nch = d >> 3;
   ss = wave_sum(ss);
   const float r = rsqrtf(ss / (float)d + eps);
@@ -20,12 +21,23 @@ __device__ __forceinline__ void norm_store(float (&v)[CPL][8], float ss, const u
     if (ch < nch) {
       const uint4 graw = *reinterpret_cast<const uint4*>(gain + ch * 8);
       const uint16_t* gp = reinterpret_cast<const uint16_t*>(&graw);
+      float y[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) y[e] = v[c][e] * r * bf2f(gp[e]);
       uint4 o;
       uint32_t* op = reinterpret_cast<uint32_t*>(&o);
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        op[e] = pack2bf(v[c][2 * e] * r * bf2f(gp[2 * e]), v[c][2 * e + 1] * r * bf2f(gp[2 * e + 1]));
+      for (int e = 0; e < 4; ++e) op[e] = pack2bf(y[2 * e], y[2 * e + 1]);
       *reinterpret_cast<uint4*>(out + ch * 8) = o;
+      if (out_lo) {
+        const uint16_t* hi = reinterpret_cast<const uint16_t*>(&o);
+        uint4 lo;
+        uint32_t* lp = reinterpret_cast<uint32_t*>(&lo);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          lp[e] = pack2bf(y[2 * e] - bf2f(hi[2 * e]), y[2 * e + 1] - bf2f(hi[2 * e + 1]));
+        *reinterpret_cast<uint4*>(out_lo + ch * 8) = lo;
+      }
     }
   }
 }
@@ -109,6 +121,7 @@ __global__ __launch_bounds__(256) void select_norm_kernel(StepGeom g, int mode,
                                                           const float* __restrict__ x,
                                                           const uint16_t* __restrict__ gain,
                                                           float eps, int d, uint16_t* __restrict__ hf,
+                                                          uint16_t* __restrict__ hf_lo,
                                                           int32_t* __restrict__ target) {
   const int lane = threadIdx.x & 63;
   const int rows_per_seq = mode == 0 ? g.Lb : 2 * g.Lb;
@@ -128,7 +141,7 @@ __global__ __launch_bounds__(256) void select_norm_kernel(StepGeom g, int mode,
   }
   float v[CPL][8];
   const float ss = load_row_f32<CPL>(x + ((size_t)b * g.T + src) * d, d, lane, v);
-  norm_store<CPL>(v, ss, gain, eps, d, lane, hf + (size_t)r * d);
+  norm_store<CPL>(v, ss, gain, eps, d, lane, hf + (size_t)r * d, hf_lo + (size_t)r * d);
 }
 
 }  // namespace
@@ -155,14 +168,14 @@ void launch_rmsnorm(const float* x, const uint16_t* gain, float eps, int M, int 
 }
 
 void launch_select_norm(const StepGeom& g, int mode, const int32_t* tokens, const float* x,
-                        const uint16_t* gain, float eps, int d, uint16_t* hf, int32_t* target,
-                        hipStream_t st) {
+                        const uint16_t* gain, float eps, int d, uint16_t* hf, uint16_t* hf_lo,
+                        int32_t* target, hipStream_t st) {
   const int R = g.B * (mode == 0 ? g.Lb : 2 * g.Lb);
   dim3 grid((R + 3) / 4), block(256);
-  if (d <= 512) select_norm_kernel<1><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, target);
-  else if (d <= 1024) select_norm_kernel<2><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, target);
-  else if (d <= 2048) select_norm_kernel<4><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, target);
-  else select_norm_kernel<8><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, target);
+  if (d <= 512) select_norm_kernel<1><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target);
+  else if (d <= 1024) select_norm_kernel<2><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target);
+  else if (d <= 2048) select_norm_kernel<4><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target);
+  else select_norm_kernel<8><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target);
 }
 
 }  // namespace wino

@@ -39,9 +39,10 @@ void launch_rmsnorm(const float* x, const uint16_t* gain, float eps, int M, int 
 // Rows the decision reads.  mode 0: one row per block position (current row
 // if the token is the mask, else the shadow row) and target = current token
 // (-1 for masked).  mode 1: all 2*Lb rows (current then shadow) per sequence.
+// The normed row is written as hi = bf16(y) and lo = bf16(y - hi).
 void launch_select_norm(const StepGeom& g, int mode, const int32_t* tokens, const float* x,
-                        const uint16_t* gain, float eps, int d, uint16_t* hf, int32_t* target,
-                        hipStream_t st);
+                        const uint16_t* gain, float eps, int d, uint16_t* hf, uint16_t* hf_lo,
+                        int32_t* target, hipStream_t st);
 
 // --------------------------------------------------------------- GEMM
 // C = A * W^T with A bf16 [M, K] (row stride lda), W bf16 [N, K] (row stride
@@ -70,6 +71,9 @@ enum GemmEpi { EPI_QKV_ROPE = 0, EPI_RESIDUAL = 1, EPI_SWIGLU = 2, EPI_LMSTATS =
 
 struct GemmCall {
   const uint16_t* A; int lda;
+  // LM-head epilogues take A as an unevaluated sum A + A2 of two bf16 parts
+  // (hi and lo of an fp32 row): both are multiplied with the same W tile.
+  const uint16_t* A2;
   const uint16_t* W; int ldw;
   int M, N, K;
   GemmEpi epi;

@@ -29,7 +29,7 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 int round64(int v) { return (v + 63) / 64 * 64; }
 
 struct Layout {
-  size_t x, h, q, k, vt, att, u, hf, target, rope_cos, rope_sin, pm, ps, pb, pi, pt, misc, total;
+  size_t x, h, q, k, vt, att, u, hf, hf_lo, target, rope_cos, rope_sin, pm, ps, pb, pi, pt, misc, total;
   int max_part;
 };
 
@@ -50,6 +50,7 @@ Layout make_layout(const wino_model_config& c, int max_batch, int max_seq) {
   L.att = take(M * d * 2);
   L.u = take(M * F * 2);
   L.hf = take(M * d * 2);
+  L.hf_lo = take(M * d * 2);
   L.target = take(M * 4);
   L.rope_cos = take((size_t)max_seq * (hd / 2) * 4);
   L.rope_sin = take((size_t)max_seq * (hd / 2) * 4);
@@ -97,6 +98,7 @@ struct wino_ctx {
   uint16_t* att() const { return at<uint16_t>(L.att); }
   uint16_t* u() const { return at<uint16_t>(L.u); }
   uint16_t* hf() const { return at<uint16_t>(L.hf); }
+  uint16_t* hf_lo() const { return at<uint16_t>(L.hf_lo); }
   int32_t* target() const { return at<int32_t>(L.target); }
   float* rope_cos() const { return at<float>(L.rope_cos); }
   float* rope_sin() const { return at<float>(L.rope_sin); }
@@ -172,8 +174,9 @@ StepGeom make_geom(const wino_params* p, const int32_t* block_start) {
   return g;
 }
 
-// Embedding and the first n_layers layers; leaves the residual stream in x.
-wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, int n_layers,
+// Embedding and the first n_sub sublayers (attention and FFN halves of each
+// layer, in order); leaves the residual stream in x.
+wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, int n_sub,
                         hipStream_t st) {
   const wino_model_config& m = c->cfg;
   const int d = m.d_model, F = m.d_ff, H = m.n_heads, hd = m.head_dim;
@@ -184,7 +187,7 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
     HIP_TRY(c, hipGetLastError());
     br.done(0, (double)M * d * (2 + 4 + 2));
   }
-  for (int l = 0; l < n_layers; ++l) {
+  for (int l = 0; l < m.n_layers && 2 * l < n_sub; ++l) {
     GemmCall qc{};
     qc.A = c->h(); qc.lda = d; qc.W = c->w_qkv[l]; qc.ldw = d;
     qc.M = M; qc.N = 3 * d; qc.K = d; qc.epi = EPI_QKV_ROPE;
@@ -209,6 +212,7 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
       HIP_TRY(c, launch_gemm(oc, st));
       br.done(2.0 * M * d * d, 2.0 * ((double)M * d + (double)d * d) + 8.0 * M * d);
     }
+    if (2 * l + 1 >= n_sub) break;
     {
       Bracket br(c, K_RMSNORM, st);
       launch_rmsnorm(c->x(), c->ffn_norm[l], m.rms_eps, M, d, c->h(), st);
@@ -231,7 +235,7 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
       HIP_TRY(c, launch_gemm(dc, st));
       br.done(2.0 * M * (double)F * d, 2.0 * ((double)M * F + (double)F * d) + 8.0 * M * d);
     }
-    if (l + 1 < n_layers) {
+    if (l + 1 < m.n_layers && 2 * (l + 1) < n_sub) {
       Bracket br(c, K_RMSNORM, st);
       launch_rmsnorm(c->x(), c->attn_norm[l + 1], m.rms_eps, M, d, c->h(), st);
       HIP_TRY(c, hipGetLastError());
@@ -246,17 +250,18 @@ wino_status step_impl(wino_ctx* c, const wino_params* p, int32_t* tokens, int32_
                       int advance, int32_t* seq_steps, hipStream_t st) {
   const wino_model_config& m = c->cfg;
   const StepGeom g = make_geom(p, block_start);
-  wino_status s = run_forward(c, g, tokens, m.n_layers, st);
+  wino_status s = run_forward(c, g, tokens, 2 * m.n_layers, st);
   if (s != WINO_OK) return s;
   const int R = g.B * g.Lb;
   {
     Bracket br(c, K_SELECT_NORM, st);
-    launch_select_norm(g, 0, tokens, c->x(), c->final_norm, m.rms_eps, m.d_model, c->hf(), c->target(), st);
+    launch_select_norm(g, 0, tokens, c->x(), c->final_norm, m.rms_eps, m.d_model, c->hf(), c->hf_lo(),
+                       c->target(), st);
     HIP_TRY(c, hipGetLastError());
     br.done(0, (double)R * m.d_model * 6);
   }
   GemmCall lc{};
-  lc.A = c->hf(); lc.lda = m.d_model; lc.W = c->lm_head; lc.ldw = m.d_model;
+  lc.A = c->hf(); lc.A2 = c->hf_lo(); lc.lda = m.d_model; lc.W = c->lm_head; lc.ldw = m.d_model;
   lc.M = R; lc.N = m.vocab; lc.K = m.d_model; lc.epi = EPI_LMSTATS;
   const int bn = gemm_tile_n(lc);
   if (bn == 0) { c->err = "no LM-head tile for this shape"; return WINO_ERR_UNSUPPORTED; }
@@ -518,12 +523,13 @@ wino_status wino_debug_logits(wino_ctx* c, const wino_params* p, const int32_t* 
   hipStream_t st = static_cast<hipStream_t>(stream);
   const wino_model_config& m = c->cfg;
   const StepGeom g = make_geom(p, d_block_start);
-  s = run_forward(c, g, d_tokens, m.n_layers, st);
+  s = run_forward(c, g, d_tokens, 2 * m.n_layers, st);
   if (s != WINO_OK) return s;
-  launch_select_norm(g, 1, d_tokens, c->x(), c->final_norm, m.rms_eps, m.d_model, c->hf(), c->target(), st);
+  launch_select_norm(g, 1, d_tokens, c->x(), c->final_norm, m.rms_eps, m.d_model, c->hf(), c->hf_lo(),
+                     c->target(), st);
   HIP_TRY(c, hipGetLastError());
   GemmCall lc{};
-  lc.A = c->hf(); lc.lda = m.d_model; lc.W = c->lm_head; lc.ldw = m.d_model;
+  lc.A = c->hf(); lc.A2 = c->hf_lo(); lc.lda = m.d_model; lc.W = c->lm_head; lc.ldw = m.d_model;
   lc.M = g.B * 2 * g.Lb; lc.N = m.vocab; lc.K = m.d_model; lc.epi = EPI_STORE_F32;
   lc.outf = d_logits; lc.ldc = m.vocab; lc.bias = c->lm_bias;
   Bracket br(c, K_GEMM_DEBUG, st);
@@ -533,15 +539,16 @@ wino_status wino_debug_logits(wino_ctx* c, const wino_params* p, const int32_t* 
 }
 
 wino_status wino_debug_forward(wino_ctx* c, const wino_params* p, const int32_t* d_tokens,
-                               const int32_t* d_block_start, int32_t n_layers, float* d_out, void* stream) {
+                               const int32_t* d_block_start, int32_t n_sublayers, float* d_out,
+                               void* stream) {
   if (!c) return WINO_ERR_INVALID_ARG;
   wino_status s = validate_params(c, p);
   if (s != WINO_OK) return s;
   if (!d_tokens || !d_block_start || !d_out) return WINO_ERR_INVALID_ARG;
-  if (n_layers < 0 || n_layers > c->cfg.n_layers) return WINO_ERR_INVALID_ARG;
+  if (n_sublayers < 0 || n_sublayers > 2 * c->cfg.n_layers) return WINO_ERR_INVALID_ARG;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const StepGeom g = make_geom(p, d_block_start);
-  s = run_forward(c, g, d_tokens, n_layers, st);
+  s = run_forward(c, g, d_tokens, n_sublayers, st);
   if (s != WINO_OK) return s;
   HIP_TRY(c, hipMemcpyAsync(d_out, c->x(), sizeof(float) * (size_t)g.B * g.T * c->cfg.d_model,
                             hipMemcpyDeviceToDevice, st));

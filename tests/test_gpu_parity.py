@@ -1,9 +1,14 @@
 """Parity of the HIP path (through the C ABI) against the float64 oracle.
 
 Every input is seeded and synthetic; oracle inputs are the same bytes the GPU
-receives.  Tolerances: logits within 2e-2 max relative error per row; decisions
-and token ids bit-exact wherever the oracle's deciding probability is more than
-1e-3 from its threshold (ids also need a top-2 gap above 1e-3).
+receives.  Tolerances: logits within 2e-2 max relative error per row against
+the float64 oracle.  Decisions and token ids are floating-point-decided
+integers, so both sides take them in the kernel's precision: the oracle runs
+with bf16 rounding at the points where the kernels materialise bf16
+activations (everything else float64), and decisions must be bit-exact
+wherever that oracle's deciding probability is more than 1e-3 from its
+threshold (ids also need a top-2 gap above 1e-3).  The probability gap to the
+float64 oracle is asserted separately.
 """
 import math
 
@@ -68,18 +73,20 @@ def oracle_params(prm_c, **kw):
                     float(np.float32(prm_c.tau1)), float(np.float32(prm_c.tau2)), prm_c.max_steps, **kw)
 
 
-def compare_step(gpu_tok, gpu_flags, r, cur, mask_id, tau1, c0, lb, label=""):
-    """Assert GPU decisions equal the oracle's where the oracle fixes them.
-    Returns how many positions were compared."""
+def compare_step(gpu_tok, gpu_flags, r, cur, mask_id, tau1, c0, lb, label="", margin=MARGIN):
+    """Assert GPU decisions equal the oracle's where the oracle fixes them:
+    deciding probability more than `margin` from its threshold (and top-2 gap
+    above `margin` for drafted ids).  Returns how many positions were compared."""
     masked = cur == mask_id
-    ok = decided_mask(r.margin, r.top2_gap, masked)
+    ok = (r.margin > margin) & ~(masked & (r.top2_gap <= margin))
     cap_now = np.any(r.flags == W.CAPFILL)
     if cap_now:
-        ok = ~masked | (r.top2_gap > MARGIN)
+        ok = ~masked | (r.top2_gap > margin)
     else:
         confm = r.conf[masked]
-        if masked.any() and not np.any(confm > tau1 + MARGIN):
-            if np.all(confm < tau1 - MARGIN) and forced_is_robust(r.conf, masked):
+        if masked.any() and not np.any(confm > tau1 + margin):
+            c = np.sort(confm)
+            if np.all(confm < tau1 - margin) and (len(c) < 2 or c[-1] - c[-2] > margin):
                 pass  # the forced draft is fixed: compare it
             else:
                 ok &= ~masked
@@ -111,8 +118,10 @@ def test_embedding_rows_are_exact(P):
     model.close()
 
 
-@pytest.mark.parametrize("n_layers", [1, 2])
-def test_residual_stream_matches_oracle(P, n_layers):
+@pytest.mark.parametrize("n_sub", [1, 2, 3, 4])
+def test_residual_stream_matches_oracle(P, n_sub):
+    """Residual stream after each sublayer: close to float64, and within
+    float32-summation noise of the oracle run in the kernel's precision."""
     cfg, w = tiny()
     wd = to_device(w)
     p, g, lb, B = 32, 64, 16, 2
@@ -122,15 +131,63 @@ def test_residual_stream_matches_oracle(P, n_layers):
     prm = P.make_params(B, p, g, lb, cfg.mask_id)
     out = torch.empty(B, p + g + lb, cfg.d_model, dtype=torch.float32, device="cuda")
     P.wino_debug_forward(model.ctx, prm, torch.tensor(tok, dtype=torch.int32, device="cuda"),
-                         torch.tensor(bstart, dtype=torch.int32, device="cuda"), n_layers, out)
+                         torch.tensor(bstart, dtype=torch.int32, device="cuda"), n_sub, out)
     torch.cuda.synchronize()
     got = out.cpu().numpy()
     for b in range(B):
         ext, pos, allowed, _ = M.extended_inputs(tok[b], p, g, lb, bstart[b], cfg.mask_id)
-        ref = M.forward_residual(w, cfg, ext, pos, allowed, n_layers=n_layers)
-        err = rowwise_rel_err(got[b], ref)
+        ref = M.forward_residual(w, cfg, ext, pos, allowed, n_sublayers=n_sub)
+        ref16 = M.forward_residual(w, cfg, ext, pos, allowed, act_round=M.round_bf16, n_sublayers=n_sub)
+        err, err16 = rowwise_rel_err(got[b], ref), rowwise_rel_err(got[b], ref16)
+        print(f"sublayers {n_sub} seq {b}: rel err vs fp64 {err:.2e}, vs bf16-point oracle {err16:.2e}")
         assert err < 1e-2, f"seq {b}: residual rel err {err}"
+        assert err16 < 2e-3, f"seq {b}: residual rel err vs kernel-precision oracle {err16}"
     model.close()
+
+
+def oracle_rows(w, cfg, ext, pos, allowed, n_sub, act_round=None, perturb=0.0, seed=0):
+    """Oracle residual after n_sub sublayers, optionally with the embedding
+    rows scaled by (1 + perturb * N(0,1)) to expose float32-level sensitivity."""
+    rows = M.f64(w["tok_emb"][torch.as_tensor(ext)])
+    if perturb:
+        rows = rows * (1.0 + perturb * np.random.default_rng(seed).standard_normal(rows.shape))
+    ws = dict(w, tok_emb=torch.from_numpy(rows))
+    return M.forward_residual(ws, cfg, np.arange(len(ext)), pos, allowed, act_round=act_round,
+                              n_sublayers=n_sub)
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("n_sub", [1, 2])
+def test_full_shape_residual_per_sublayer(P, n_sub):
+    """At the 8B shape the bf16 rounding points make the forward sensitive:
+    float32-level input noise (1e-7) already moves the kernel-precision oracle
+    by ~1e-3.  The GPU must agree with that oracle as well as the oracle
+    agrees with itself under such noise, and stay within 1.5e-2 of float64."""
+    cfg, wd = big_one_layer("llada8b")
+    B, p, g, lb = 1, 256, 256, 32
+    model = P.WinoModel(cfg, wd, B, p + g + lb)
+    pr = wi.prompts(cfg, B, p, seed=1).numpy()
+    tok = np.concatenate([pr, np.full((B, g), cfg.mask_id)], axis=1).astype(np.int64)
+    tok[0, p:p + 48] = np.random.default_rng(0).integers(0, cfg.mask_id, 48)
+    prm = P.make_params(B, p, g, lb, cfg.mask_id)
+    out = torch.empty(B, p + g + lb, cfg.d_model, dtype=torch.float32, device="cuda")
+    P.wino_debug_forward(model.ctx, prm, torch.tensor(tok, dtype=torch.int32, device="cuda"),
+                         torch.tensor([32], dtype=torch.int32, device="cuda"), n_sub, out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()[0]
+    model.close()
+    w = to_cpu(wd)
+    del wd
+    ext, pos, allowed, _ = M.extended_inputs(tok[0], p, g, lb, 32, cfg.mask_id)
+    ref = oracle_rows(w, cfg, ext, pos, allowed, n_sub)
+    ref16 = oracle_rows(w, cfg, ext, pos, allowed, n_sub, M.round_bf16)
+    ref16p = oracle_rows(w, cfg, ext, pos, allowed, n_sub, M.round_bf16, perturb=1e-7)
+    err, err16, chaos = (rowwise_rel_err(got, ref), rowwise_rel_err(got, ref16),
+                         rowwise_rel_err(ref16p, ref16))
+    print(f"8B shape, sublayers {n_sub}: vs fp64 {err:.2e}, vs bf16-point {err16:.2e}, "
+          f"oracle self-sensitivity {chaos:.2e}")
+    assert err < 1.5e-2
+    assert err16 < 3 * chaos + 1e-4
 
 
 @pytest.mark.parametrize("variant", ["literal", "wide"])
@@ -186,7 +243,9 @@ def test_teacher_forced_steps(P, variant, tau1, tau2):
     prm_c = P.make_params(2, p, g, lb, cfg.mask_id, tau1, tau2)
     prm = oracle_params(prm_c)
     tok0 = batch_tokens(cfg, 2, p, g, seed=5)
-    trajs = [oracle_trajectory(W.ModelProvider(w, cfg), tok0[b], prm)[0] for b in range(2)]
+    prov = W.ModelProvider(w, cfg, act_round=M.round_bf16)
+    prov64 = W.ModelProvider(w, cfg)
+    trajs = [oracle_trajectory(prov, tok0[b], prm)[0] for b in range(2)]
     n_cmp = 0
     for k in range(max(len(t) for t in trajs)):
         states = [t[min(k, len(t) - 1)] for t in trajs]
@@ -207,7 +266,9 @@ def test_teacher_forced_steps(P, variant, tau1, tau2):
             masked = cur == cfg.mask_id
             val = np.exp(np.where(masked, gstats["z_best"][b], gstats["z_target"][b]) - gstats["m_all"][b]) / gstats["sumexp"][b]
             ref = np.where(masked, r.conf, r.s)
-            assert np.max(np.abs(val - ref)) < 2e-2
+            assert np.max(np.abs(val - ref)) < 5e-3
+            r64 = W.step(prov64, tb, prm, bs, steps)
+            assert np.max(np.abs(val - np.where(masked, r64.conf, r64.s))) < 2e-2
             assert np.array_equal(gstats["row_kind"][b], np.where(masked, 0, 1))
     assert n_cmp > 0
     model.close()
@@ -234,7 +295,7 @@ def test_decode_matches_oracle(P, variant, tau1, tau2, lb):
     assert np.array_equal(got[:, :p], tok0[:, :p])
     assert forwards == max(steps)
     for b in range(B):
-        traj, final = oracle_trajectory(W.ModelProvider(w, cfg), tok0[b], prm)
+        traj, final = oracle_trajectory(W.ModelProvider(w, cfg, act_round=M.round_bf16), tok0[b], prm)
         robust = all(np.all(decided_mask(r.margin, r.top2_gap, t[c0:c0 + lb] == cfg.mask_id))
                      and (not np.any(r.flags == W.FORCED)
                           or forced_is_robust(r.conf, t[c0:c0 + lb] == cfg.mask_id))
@@ -351,10 +412,61 @@ def test_full_shape_one_layer_step(P, name, B, p, g, lb, check, image):
     model.close()
     del wd
     for b in check:
-        prov = W.ModelProvider(w, cfg)
-        r = W.step(prov, tok0[b], prm, bstart[b], 1)
-        c0 = p + bstart[b]
-        err = rowwise_rel_err(logits[b].cpu().numpy(), np.concatenate([r.z_cur, r.z_shad]))
-        assert err < LOGIT_TOL, f"seq {b}: logits rel err {err}"
-        n = compare_step(gt[b], gf[b], r, tok0[b][c0:c0 + lb], cfg.mask_id, prm.tau1, c0, lb, f"seq {b}")
-        assert n > 0
+        r64 = W.step(W.ModelProvider(w, cfg), tok0[b], prm, bstart[b], 1)
+        r16 = W.step(W.ModelProvider(w, cfg, act_round=M.round_bf16), tok0[b], prm, bstart[b], 1)
+        check_full_step(b, gt, gf, gstats, logits[b].cpu().numpy(), r64, r16, tok0[b], p, lb, cfg, prm,
+                        bstart[b])
+
+
+def check_full_step(b, gt, gf, gstats, logits_b, r64, r16, tok_b, p, lb, cfg, prm, bstart_b):
+    """Decisions at the full shape.  delta = the largest gap, over the block,
+    between the float64 oracle's deciding probability and the same oracle run
+    at the kernel's bf16 rounding points (oracle data only): the precision the
+    kernel's arithmetic has.  Decisions must match wherever the float64
+    margin exceeds max(1e-3, 2*delta); the GPU's probabilities must be within
+    3*delta (+1e-4) of float64."""
+    c0 = p + bstart_b
+    cur = tok_b[c0:c0 + lb]
+    masked = cur == cfg.mask_id
+    err = rowwise_rel_err(logits_b, np.concatenate([r64.z_cur, r64.z_shad]))
+    assert err < LOGIT_TOL, f"seq {b}: logits rel err {err}"
+    p64 = np.where(masked, r64.conf, r64.s)
+    delta = float(np.max(np.abs(p64 - np.where(masked, r16.conf, r16.s))))
+    val = np.exp(np.where(masked, gstats["z_best"][b], gstats["z_target"][b]) - gstats["m_all"][b]) / gstats["sumexp"][b]
+    dp64 = float(np.max(np.abs(val - p64)))
+    margin = max(MARGIN, 2 * delta)
+    n = compare_step(gt[b], gf[b], r64, cur, cfg.mask_id, prm.tau1, c0, lb, f"seq {b}", margin=margin)
+    print(f"seq {b}: logits err {err:.2e}; kernel-precision delta {delta:.2e}; GPU |dp| vs fp64 {dp64:.2e}; "
+          f"{n}/{lb} decisions compared at margin {margin:.2e}")
+    assert dp64 <= 3 * delta + 1e-4
+    assert n > 0
+
+
+@pytest.mark.slow
+def test_full_model_step_bs1_literal(P):
+    """All 32 layers at the 8B shape, batch 1, literal init (the benchmark's
+    bs1 configuration); the oracle runs the whole step for the sequence."""
+    cfg = wi.preset("llada8b")
+    wd = wi.model_weights(cfg, seed=0, device="cuda")
+    B, p, g, lb = 1, 256, 256, 32
+    model = P.WinoModel(cfg, wd, B, p + g + lb)
+    prm_c = P.make_params(B, p, g, lb, cfg.mask_id, 0.7, 0.9)
+    prm = oracle_params(prm_c)
+    pr = wi.prompts(cfg, B, p, seed=1000).numpy()
+    tok0 = np.concatenate([pr, np.full((B, g), cfg.mask_id)], axis=1).astype(np.int64)
+    rng = np.random.default_rng(3)
+    tok0[0, p:p + lb] = rng.integers(0, cfg.mask_id, lb)
+    sel = np.arange(p + lb, p + 2 * lb)[rng.random(lb) < 0.5]
+    tok0[0, sel] = rng.integers(0, cfg.mask_id, len(sel))
+    gt, gf, gnm, gst, gstats = gpu_step(P, model, prm_c, tok0, [lb], [1])
+    logits = torch.empty(B, 2 * lb, cfg.vocab, dtype=torch.float32, device="cuda")
+    P.wino_debug_logits(model.ctx, prm_c, torch.tensor(tok0, dtype=torch.int32, device="cuda"),
+                        torch.tensor([lb], dtype=torch.int32, device="cuda"), logits)
+    torch.cuda.synchronize()
+    model.close()
+    w = to_cpu(wd)
+    del wd
+    torch.cuda.empty_cache()
+    r64 = W.step(W.ModelProvider(w, cfg), tok0[0], prm, lb, 1)
+    r16 = W.step(W.ModelProvider(w, cfg, act_round=M.round_bf16), tok0[0], prm, lb, 1)
+    check_full_step(0, gt, gf, gstats, logits[0].cpu().numpy(), r64, r16, tok0[0], p, lb, cfg, prm, lb)
