@@ -120,8 +120,10 @@ def test_embedding_rows_are_exact(P):
 
 @pytest.mark.parametrize("n_sub", [1, 2, 3, 4])
 def test_residual_stream_matches_oracle(P, n_sub):
-    """Residual stream after each sublayer: close to float64, and within
-    float32-summation noise of the oracle run in the kernel's precision."""
+    """Residual stream after each sublayer: close to float64, and as close to
+    the oracle run at the kernel's bf16 rounding points as that oracle is to
+    itself under float32-level input noise (its rounding points make it
+    sensitive: a 1e-7 input change moves it by up to ~3e-3 here)."""
     cfg, w = tiny()
     wd = to_device(w)
     p, g, lb, B = 32, 64, 16, 2
@@ -133,16 +135,22 @@ def test_residual_stream_matches_oracle(P, n_sub):
     P.wino_debug_forward(model.ctx, prm, torch.tensor(tok, dtype=torch.int32, device="cuda"),
                          torch.tensor(bstart, dtype=torch.int32, device="cuda"), n_sub, out)
     torch.cuda.synchronize()
+    model.close()
     got = out.cpu().numpy()
+    errs, errs16, chaos = [], [], 0.0
     for b in range(B):
         ext, pos, allowed, _ = M.extended_inputs(tok[b], p, g, lb, bstart[b], cfg.mask_id)
-        ref = M.forward_residual(w, cfg, ext, pos, allowed, n_sublayers=n_sub)
-        ref16 = M.forward_residual(w, cfg, ext, pos, allowed, act_round=M.round_bf16, n_sublayers=n_sub)
-        err, err16 = rowwise_rel_err(got[b], ref), rowwise_rel_err(got[b], ref16)
-        print(f"sublayers {n_sub} seq {b}: rel err vs fp64 {err:.2e}, vs bf16-point oracle {err16:.2e}")
-        assert err < 1e-2, f"seq {b}: residual rel err {err}"
-        assert err16 < 2e-3, f"seq {b}: residual rel err vs kernel-precision oracle {err16}"
-    model.close()
+        ref = oracle_rows(w, cfg, ext, pos, allowed, n_sub)
+        ref16 = oracle_rows(w, cfg, ext, pos, allowed, n_sub, M.round_bf16)
+        for seed in (1, 2):
+            ref16p = oracle_rows(w, cfg, ext, pos, allowed, n_sub, M.round_bf16, perturb=1e-7, seed=seed)
+            chaos = max(chaos, rowwise_rel_err(ref16p, ref16))
+        errs.append(rowwise_rel_err(got[b], ref))
+        errs16.append(rowwise_rel_err(got[b], ref16))
+    print(f"sublayers {n_sub}: rel err vs fp64 {max(errs):.2e}, vs bf16-point {max(errs16):.2e}, "
+          f"oracle self-sensitivity {chaos:.2e}")
+    assert max(errs) < 1e-2
+    assert max(errs16) < 3 * chaos + 1e-4
 
 
 def oracle_rows(w, cfg, ext, pos, allowed, n_sub, act_round=None, perturb=0.0, seed=0):
