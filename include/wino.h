@@ -179,6 +179,13 @@ wino_status wino_debug_forward(wino_ctx* ctx, const wino_params* p, const int32_
                                const int32_t* d_block_start, int32_t n_sublayers, float* d_out,
                                void* stream);
 
+/* wino_debug_gemm: out fp32 [M, N] = A W^T for bf16 A [M, K] and W [N, K]
+ *   (row-major, contiguous), the backbone GEMM kernel with a plain store.
+ *   K must be a multiple of 64 and N of the tile width (128); otherwise
+ *   WINO_ERR_UNSUPPORTED.  Asynchronous on `stream`. */
+wino_status wino_debug_gemm(const void* d_A, const void* d_W, int32_t M, int32_t N, int32_t K,
+                            float* d_out, void* stream);
+
 /* Kernel timing with HIP events on the launch stream.  enable != 0 records a
  * pair of events around every launch of the kernel classes in `class_mask`
  * (bit i = class i, see wino_kernel_class_name).  wino_profile_read

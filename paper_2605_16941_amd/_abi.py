@@ -27,7 +27,7 @@ def _load():
     if not os.path.exists(_LIB_PATH):
         raise ImportError(
             f"libwino.so not found at {_LIB_PATH}; build it with "
-            "`python -m paper_2605_16941_amd.build` (hipcc, gfx950)")
+            "`python paper_2605_16941_amd/build.py` (hipcc, gfx950)")
     return C.CDLL(_LIB_PATH)
 
 
@@ -81,6 +81,7 @@ _protos = {
     "wino_epilogue": (_i32, [_P(wino_params), _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "wino_debug_logits": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _vp]),
     "wino_debug_forward": (_i32, [_vp, _P(wino_params), _vp, _vp, _i32, _vp, _vp]),
+    "wino_debug_gemm": (_i32, [_vp, _vp, _i32, _i32, _i32, _vp, _vp]),
     "wino_profile": (_i32, [_vp, _u32]),
     "wino_profile_read": (_i32, [_vp, _P(C.c_int64), _P(C.c_double), _P(C.c_double), _P(C.c_double)]),
     "wino_kernel_class_name": (C.c_char_p, [_i32]),
@@ -215,6 +216,17 @@ def wino_debug_forward(ctx, p: wino_params, tokens, block_start, n_sublayers, ou
                                   _ptr(block_start, torch.int32, "block_start"), n_sublayers,
                                   _ptr(out, torch.float32, "out"), _stream(stream)),
            "wino_debug_forward", ctx)
+
+
+def wino_debug_gemm(A, W, out, stream=None) -> None:
+    """out = A W^T (fp32) with the backbone GEMM kernel; A [M,K], W [N,K] bf16."""
+    import torch
+    M, K = A.shape
+    N = W.shape[0]
+    if W.shape[1] != K or tuple(out.shape) != (M, N):
+        raise ValueError("wino_debug_gemm: shape mismatch")
+    _check(lib.wino_debug_gemm(_ptr(A, torch.bfloat16, "A"), _ptr(W, torch.bfloat16, "W"), M, N, K,
+                               _ptr(out, torch.float32, "out"), _stream(stream)), "wino_debug_gemm")
 
 
 def wino_profile(ctx, class_mask: int) -> None:

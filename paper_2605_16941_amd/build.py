@@ -1,6 +1,6 @@
 """Build libwino.so (HIP for gfx950) in place, next to this file.
 
-    python -m paper_2605_16941_amd.build [--jobs N]
+    python paper_2605_16941_amd/build.py [--jobs N]
 
 Every source is compiled by hipcc for gfx950 only, with packed-fp32 vector
 instructions disabled, then linked into one shared library exporting the C ABI

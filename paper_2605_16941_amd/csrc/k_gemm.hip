@@ -21,6 +21,7 @@
 // so that each XCD works on one contiguous range of tiles (shared W tiles stay
 // in that XCD's L2).
 #include <climits>
+#include <cstdlib>
 
 #include "common.h"
 #include "kernels.h"
@@ -222,7 +223,7 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int FM = WTM / 32, FN = WTN / 32;
   // LM-head epilogues multiply W with both bf16 parts (hi, lo) of the fp32 rows
-  constexpr bool SPLIT = EPI == EPI_LMSTATS || EPI == EPI_STORE_F32;
+  constexpr bool SPLIT = EPI == EPI_LMSTATS || EPI == EPI_LOGITS;
   constexpr int AROWS = SPLIT ? 2 * BM : BM;
   // one LDS-DMA instruction moves 64 lanes x 16 bytes = 8 tile rows of 64 bf16
   constexpr int A_INS = AROWS / (8 * NW);
@@ -248,14 +249,19 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
   const int m0 = tm * BM, n0 = tn * BN;
 
   // Tile rows are 128 bytes = 8 chunks of 16 bytes; chunk kc of row r is
-  // stored at position kc ^ (r & 7).  The lane that fills position (lane & 7)
-  // of row (8*i + lane/8) therefore fetches chunk (lane & 7) ^ (lane >> 3).
+  // stored at position kc ^ swz(r), swz(r) = (r ^ (r >> 3)) & 7.  Any 8
+  // consecutive rows then use 8 different positions, and any 16 consecutive
+  // rows 16 different (row parity, position) pairs: the fragment reads of a
+  // wave hit distinct LDS banks whether 8 or 16 lanes are served per cycle.
+  // The lane that fills position (lane & 7) of row 8*i + lane/8 of a tile
+  // therefore fetches chunk (lane & 7) ^ ((lane/8 ^ i) & 7).
   const int lrow = lane >> 3;
-  const int lkc = (lane & 7) ^ lrow;
   const uint16_t* asrc[A_INS];
 #pragma unroll
   for (int i = 0; i < A_INS; ++i) {
-    const int row = (wave * A_INS + i) * 8 + lrow;
+    const int gi = wave * A_INS + i;
+    const int row = gi * 8 + lrow;
+    const int lkc = (lane & 7) ^ ((lrow ^ gi) & 7);
     const bool lo = SPLIT && row >= BM;
     const int gm = min(m0 + (lo ? row - BM : row), c.M - 1);
     asrc[i] = (lo ? c.A2 : c.A) + (size_t)gm * c.lda + lkc * 8;
@@ -263,7 +269,9 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
   const uint16_t* bsrc[B_INS];
 #pragma unroll
   for (int i = 0; i < B_INS; ++i) {
-    const int vc = n0 + (wave * B_INS + i) * 8 + lrow;
+    const int gi = wave * B_INS + i;
+    const int lkc = (lane & 7) ^ ((lrow ^ gi) & 7);
+    const int vc = n0 + gi * 8 + lrow;
     const int wr = EPI == EPI_SWIGLU ? swiglu_row<WTN>(vc, c.F) : vc;
     bsrc[i] = c.W + (size_t)wr * c.ldw + lkc * 8;
   }
@@ -292,49 +300,112 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
       for (int i = 0; i < 16; ++i) acc[fm][fn][i] = 0.f;
 
   const int nk = c.K / BK;
-  const int swz = lane & 7;  // == row & 7 for every fragment row this lane reads
   const int arow = wm * WTM + (lane & 31), brow = wn * WTN + (lane & 31);
-  issue(0, 0);
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) {
-      issue(kt + 1, (kt + 1) & 1);
-      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(A_INS + B_INS) : "memory");
-    } else {
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    }
-    __syncthreads();
-    const uint16_t* sA = smem + (kt & 1) * STAGE;
-    const uint16_t* sB = sA + AROWS * BK;
+  // swizzle of each fragment row this lane reads (fixed over the K loop)
+  int aswz[FM], alswz[SPLIT ? FM : 1], bswz[FN];
 #pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int kc = ((ks * 2 + (lane >> 5)) ^ swz) * 8;
-      bf16x8 af[FM], bf[FN];
-#pragma unroll
-      for (int fm = 0; fm < FM; ++fm)
-        af[fm] = as_bf16x8(*reinterpret_cast<const uint4*>(sA + (arow + fm * 32) * BK + kc));
-#pragma unroll
-      for (int fn = 0; fn < FN; ++fn)
-        bf[fn] = as_bf16x8(*reinterpret_cast<const uint4*>(sB + (brow + fn * 32) * BK + kc));
-#pragma unroll
-      for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-        for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma32(af[fm], bf[fn], acc[fm][fn]);
-      if constexpr (SPLIT) {
-#pragma unroll
-        for (int fm = 0; fm < FM; ++fm)
-          af[fm] = as_bf16x8(*reinterpret_cast<const uint4*>(sA + (BM + arow + fm * 32) * BK + kc));
-#pragma unroll
-        for (int fm = 0; fm < FM; ++fm)
-#pragma unroll
-          for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma32(af[fm], bf[fn], acc[fm][fn]);
-      }
-    }
-    __syncthreads();
+  for (int fm = 0; fm < FM; ++fm) {
+    const int r = arow + fm * 32;
+    aswz[fm] = (r ^ (r >> 3)) & 7;
+    if constexpr (SPLIT) alswz[fm] = ((BM + r) ^ ((BM + r) >> 3)) & 7;
   }
+#pragma unroll
+  for (int fn = 0; fn < FN; ++fn) {
+    const int r = brow + fn * 32;
+    bswz[fn] = (r ^ (r >> 3)) & 7;
+  }
+  constexpr int KS = BK / 16;
+  constexpr int NR = FM + FN + (SPLIT ? FM : 0);   // LDS fragment reads per 16-deep step
+  constexpr int NM = FM * FN * (SPLIT ? 2 : 1);     // MFMAs per step
+  constexpr int RI = NR < NM ? NR : NM;              // reads interleaved with MFMAs
+  static_assert(KS % 2 == 0, "fragment buffers alternate per step");
+
+  bf16x8 af[2][FM], bf[2][FN], al[2][SPLIT ? FM : 1];
+  auto load_frags = [&](const uint16_t* sA, int ks, int buf) {
+    const uint16_t* sB = sA + AROWS * BK;
+    const int kc = ks * 2 + (lane >> 5);
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+      af[buf][fm] = as_bf16x8(*reinterpret_cast<const uint4*>(
+          sA + (arow + fm * 32) * BK + ((kc ^ aswz[fm]) << 3)));
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn)
+      bf[buf][fn] = as_bf16x8(*reinterpret_cast<const uint4*>(
+          sB + (brow + fn * 32) * BK + ((kc ^ bswz[fn]) << 3)));
+    if constexpr (SPLIT) {
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+        al[buf][fm] = as_bf16x8(*reinterpret_cast<const uint4*>(
+            sA + (BM + arow + fm * 32) * BK + ((kc ^ alswz[fm]) << 3)));
+    }
+  };
+  auto mfmas = [&](int buf) {
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma32(af[buf][fm], bf[buf][fn], acc[fm][fn]);
+    if constexpr (SPLIT) {
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma32(al[buf][fm], bf[buf][fn], acc[fm][fn]);
+    }
+  };
+  // steps 0..KS-2 of a tile: the reads of step ks+1 go between the MFMAs of ks
+  auto inner_steps = [&](const uint16_t* sA) {
+#pragma unroll
+    for (int ks = 0; ks + 1 < KS; ++ks) {
+      load_frags(sA, ks + 1, (ks + 1) & 1);
+      mfmas(ks & 1);
+    }
+#pragma unroll
+    for (int ks = 0; ks + 1 < KS; ++ks) {
+#pragma unroll
+      for (int r = 0; r < RI; ++r) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      if (NR > RI) __builtin_amdgcn_sched_group_barrier(0x100, NR - RI, 0);
+      if (NM > RI) __builtin_amdgcn_sched_group_barrier(0x008, NM - RI, 0);
+    }
+  };
+
+  // Pipeline: tile t sits in LDS stage t&1; its DMA is issued two tiles
+  // ahead.  Crossing from tile t to t+1, each wave (1) waits for its copies
+  // of tile t+1, (2) meets the others at the barrier - after which every
+  // wave has read all of tile t, (3) issues tile t+2 into tile t's stage,
+  // (4) issues the first fragment reads of tile t+1, and only then (5) runs
+  // the last MFMAs of tile t, which cover the latency of those reads.
+  issue(0, 0);
+  if (nk > 1) {
+    issue(1, 1);
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(A_INS + B_INS) : "memory");
+  } else {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+  __syncthreads();
+  load_frags(smem, 0, 0);
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    const uint16_t* sA = smem + (kt & 1) * STAGE;
+    inner_steps(sA);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    issue(kt + 2 < nk ? kt + 2 : nk - 1, kt & 1);  // the last one only refetches
+    load_frags(smem + ((kt + 1) & 1) * STAGE, 0, 0);
+    mfmas((KS - 1) & 1);
+    __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+  }
+  inner_steps(smem + ((nk - 1) & 1) * STAGE);
+  mfmas((KS - 1) & 1);
+  // the refetch issued last may still be landing: finish it before the
+  // epilogue reuses LDS
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
 
   const int rowb = m0 + wm * WTM, colb = n0 + wn * WTN;
   if constexpr (EPI == EPI_RESIDUAL) epi_residual<FM, FN>(c, acc, rowb, colb, lane);
-  else if constexpr (EPI == EPI_STORE_F32) epi_store<FM, FN>(c, acc, rowb, colb, lane);
+  else if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_LOGITS) epi_store<FM, FN>(c, acc, rowb, colb, lane);
   else if constexpr (EPI == EPI_SWIGLU) epi_swiglu<FM, FN>(c, acc, rowb, colb, lane);
   else if constexpr (EPI == EPI_QKV_ROPE) epi_qkv_rope<FM, FN>(c, acc, rowb, colb, lane);
   else epi_lmstats<BM, WM, WN, FM, FN>(c, acc, m0, tn, rowb, colb, lane, wm, wn, smem);
@@ -342,39 +413,57 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
 
 struct TileCfg {
   int BM, BN, WM, WN;
-  int occ;     // workgroups a CU holds at once (registers / LDS)
-  float eff;   // relative per-CU matrix-core efficiency when full
+  int occ;     // workgroups a CU holds at once (LDS / registers)
+  float eff;   // relative per-CU matrix-core throughput when the chip is full
+               // (measured on the 8704x24576x4096 gate/up shape)
 };
 
 constexpr TileCfg kTiles[] = {
-    {256, 256, 2, 2, 1, 1.00f},
-    {192, 256, 2, 2, 1, 0.97f},
-    {128, 256, 2, 2, 1, 0.90f},
-    {128, 128, 2, 2, 2, 0.80f},
-    {64, 128, 2, 2, 3, 0.60f},
-    {32, 256, 1, 4, 2, 0.50f},
+    {256, 256, 2, 2, 1, 0.94f},  // 0
+    {192, 256, 2, 2, 1, 0.90f},  // 1
+    {128, 256, 2, 2, 1, 0.75f},  // 2
+    {128, 128, 2, 2, 2, 0.77f},  // 3
+    {64, 128, 2, 2, 3, 0.65f},   // 4
+    {32, 256, 1, 4, 2, 0.95f},   // 5
+    {256, 256, 4, 2, 1, 1.00f},  // 6  (8 waves)
+    {256, 256, 2, 4, 1, 0.99f},  // 7  (8 waves)
+    {128, 256, 2, 4, 1, 0.76f},  // 8  (8 waves)
 };
+constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
+
+// Which epilogues each tile is built for.  The LM-head epilogues double the A
+// tile (hi and lo parts), which fits LDS only for BM <= 128; the thin 32-row
+// tile serves only them (it loses to wider tiles elsewhere); the 4-wave
+// 256x256 tile spills registers in the RoPE epilogue.  (RoPE also needs a
+// wave to own exactly one head, WTN == hd: checked per call.)
+constexpr bool tile_epi(int BM, int BN, int WM, int WN, int EPI) {
+  return (EPI == EPI_LMSTATS || EPI == EPI_LOGITS)
+             ? (BM == 32 || (BM == 128 && BN == 256 && WM == 2 && WN == 2))
+             : (BM != 32 && (EPI == EPI_QKV_ROPE ? !(BM == 256 && WM == 2 && WN == 2) : true));
+}
 
 bool tile_ok(const GemmCall& c, const TileCfg& t) {
   if (c.N % t.BN || c.K % BK) return false;
+  if (!tile_epi(t.BM, t.BN, t.WM, t.WN, c.epi)) return false;
   const int WTN = t.BN / t.WN;
-  const bool lm = c.epi == EPI_LMSTATS || c.epi == EPI_STORE_F32;
-  if (lm) return t.BM == 32 || (t.BM == 128 && t.BN == 256);
-  if (t.BM == 32) return false;
-  switch (c.epi) {
-    case EPI_QKV_ROPE:
-      return t.BM != 256 && t.BM != 192 && WTN == c.rope.hd && (c.rope.H * c.rope.hd) % t.BN == 0;
-    case EPI_SWIGLU:
-      return (c.F % (WTN / 2)) == 0;
-    default:
-      return true;
-  }
+  if (c.epi == EPI_QKV_ROPE) return WTN == c.rope.hd && (c.rope.H * c.rope.hd) % t.BN == 0;
+  if (c.epi == EPI_SWIGLU) return (c.F % (WTN / 2)) == 0;
+  return true;
 }
 
+int forced_tile() {
+  const char* e = std::getenv("WINO_GEMM_TILE");
+  return e ? std::atoi(e) : -1;
+}
+
+// Estimated time: waves of workgroups over 256 CUs, each CU running up to
+// `occ` tiles at once at its measured relative throughput.
 int pick_tile(const GemmCall& c) {
+  const int f = forced_tile();
+  if (f >= 0 && f < kNumTiles && tile_ok(c, kTiles[f])) return f;
   int best = -1;
   double best_t = 0;
-  for (int i = 0; i < (int)(sizeof(kTiles) / sizeof(kTiles[0])); ++i) {
+  for (int i = 0; i < kNumTiles; ++i) {
     const TileCfg& t = kTiles[i];
     if (!tile_ok(c, t)) continue;
     const long tiles = (long)((c.M + t.BM - 1) / t.BM) * (c.N / t.BN);
@@ -387,20 +476,9 @@ int pick_tile(const GemmCall& c) {
   return best;
 }
 
-// (tile, epilogue) pairs that are built: the LM-head epilogues double the A
-// tile (hi and lo parts), which only fits LDS for BM <= 128, and the RoPE
-// epilogue needs a wave to own a whole head and spills at 256x256.
-template <int BM, int BN, int EPI>
-constexpr bool built() {
-  if (EPI == EPI_LMSTATS || EPI == EPI_STORE_F32) return BM == 32 || (BM == 128 && BN == 256);
-  if (BM == 32) return false;
-  if (EPI == EPI_QKV_ROPE) return BM != 256 && BM != 192;
-  return true;
-}
-
 template <int BM, int BN, int WM, int WN, int EPI>
 hipError_t launch_one(const GemmCall& c, hipStream_t st) {
-  if constexpr (built<BM, BN, EPI>()) {
+  if constexpr (tile_epi(BM, BN, WM, WN, EPI)) {
     const int tiles = ((c.M + BM - 1) / BM) * (c.N / BN);
     gemm_kernel<BM, BN, WM, WN, EPI><<<dim3(tiles), dim3(WM * WN * 64), 0, st>>>(c);
     return hipGetLastError();
@@ -417,6 +495,7 @@ hipError_t launch_cfg(const GemmCall& c, hipStream_t st) {
     case EPI_SWIGLU: return launch_one<BM, BN, WM, WN, EPI_SWIGLU>(c, st);
     case EPI_LMSTATS: return launch_one<BM, BN, WM, WN, EPI_LMSTATS>(c, st);
     case EPI_STORE_F32: return launch_one<BM, BN, WM, WN, EPI_STORE_F32>(c, st);
+    case EPI_LOGITS: return launch_one<BM, BN, WM, WN, EPI_LOGITS>(c, st);
   }
   return hipErrorInvalidValue;
 }
@@ -439,6 +518,9 @@ hipError_t launch_gemm(const GemmCall& c, hipStream_t st) {
     case 3: return launch_cfg<128, 128, 2, 2>(c, st);
     case 4: return launch_cfg<64, 128, 2, 2>(c, st);
     case 5: return launch_cfg<32, 256, 1, 4>(c, st);
+    case 6: return launch_cfg<256, 256, 4, 2>(c, st);
+    case 7: return launch_cfg<256, 256, 2, 4>(c, st);
+    case 8: return launch_cfg<128, 256, 2, 4>(c, st);
   }
   return hipErrorInvalidValue;
 }

@@ -67,7 +67,11 @@ struct LmStatsOut {   // LM head + streaming softmax statistics per (row, N-tile
   float* pt;          // [M, n_part] logit of target (kNegBig if not in tile)
 };
 
-enum GemmEpi { EPI_QKV_ROPE = 0, EPI_RESIDUAL = 1, EPI_SWIGLU = 2, EPI_LMSTATS = 3, EPI_STORE_F32 = 4 };
+enum GemmEpi {
+  EPI_QKV_ROPE = 0, EPI_RESIDUAL = 1, EPI_SWIGLU = 2, EPI_LMSTATS = 3,
+  EPI_STORE_F32 = 4,  // out = A W^T (plain bf16 A)
+  EPI_LOGITS = 5      // out = (A + A2) W^T + bias (LM-head precision, test entry point)
+};
 
 struct GemmCall {
   const uint16_t* A; int lda;
@@ -86,7 +90,8 @@ struct GemmCall {
   LmStatsOut lm;
 };
 // Picks a tile shape for the problem; returns the N-tile width used (the LM
-// head needs it to size its partials) or 0 if no kernel fits.
+// head needs it to size its partials) or 0 if no kernel fits.  The
+// environment variable WINO_GEMM_TILE=<index> forces one tile shape (tuning).
 int gemm_tile_n(const GemmCall& c);
 hipError_t launch_gemm(const GemmCall& c, hipStream_t st);
 

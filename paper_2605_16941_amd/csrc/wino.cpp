@@ -530,7 +530,7 @@ wino_status wino_debug_logits(wino_ctx* c, const wino_params* p, const int32_t* 
   HIP_TRY(c, hipGetLastError());
   GemmCall lc{};
   lc.A = c->hf(); lc.A2 = c->hf_lo(); lc.lda = m.d_model; lc.W = c->lm_head; lc.ldw = m.d_model;
-  lc.M = g.B * 2 * g.Lb; lc.N = m.vocab; lc.K = m.d_model; lc.epi = EPI_STORE_F32;
+  lc.M = g.B * 2 * g.Lb; lc.N = m.vocab; lc.K = m.d_model; lc.epi = EPI_LOGITS;
   lc.outf = d_logits; lc.ldc = m.vocab; lc.bias = c->lm_bias;
   Bracket br(c, K_GEMM_DEBUG, st);
   HIP_TRY(c, launch_gemm(lc, st));
@@ -553,6 +553,18 @@ wino_status wino_debug_forward(wino_ctx* c, const wino_params* p, const int32_t*
   HIP_TRY(c, hipMemcpyAsync(d_out, c->x(), sizeof(float) * (size_t)g.B * g.T * c->cfg.d_model,
                             hipMemcpyDeviceToDevice, st));
   return WINO_OK;
+}
+
+wino_status wino_debug_gemm(const void* d_A, const void* d_W, int32_t M, int32_t N, int32_t K,
+                            float* d_out, void* stream) {
+  if (!d_A || !d_W || !d_out) return WINO_ERR_INVALID_ARG;
+  if (M < 1 || N < 1 || K < 1) return WINO_ERR_SHAPE;
+  GemmCall gc{};
+  gc.A = static_cast<const uint16_t*>(d_A); gc.lda = K;
+  gc.W = static_cast<const uint16_t*>(d_W); gc.ldw = K;
+  gc.M = M; gc.N = N; gc.K = K; gc.epi = EPI_STORE_F32; gc.outf = d_out; gc.ldc = N;
+  if (gemm_tile_n(gc) == 0) return WINO_ERR_UNSUPPORTED;
+  return launch_gemm(gc, static_cast<hipStream_t>(stream)) == hipSuccess ? WINO_OK : WINO_ERR_HIP;
 }
 
 wino_status wino_profile(wino_ctx* c, uint32_t class_mask) {

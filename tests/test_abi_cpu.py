@@ -14,8 +14,8 @@ HEADER = os.path.join(ROOT, "include", "wino.h")
 def abi():
     lib_path = os.path.join(ROOT, "paper_2605_16941_amd", "libwino.so")
     if not os.path.exists(lib_path):
-        from paper_2605_16941_amd import build
-        build.build()
+        import __graft_entry__
+        __graft_entry__._load_build_module().build()
     from paper_2605_16941_amd import _abi
     return _abi
 
