@@ -256,6 +256,7 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
   // The lane that fills position (lane & 7) of row 8*i + lane/8 of a tile
   // therefore fetches chunk (lane & 7) ^ ((lane/8 ^ i) & 7).
   const int lrow = lane >> 3;
+  const int kbase = blockIdx.y * c.K;  // split-K: this split's first column
   const uint16_t* asrc[A_INS];
 #pragma unroll
   for (int i = 0; i < A_INS; ++i) {
@@ -264,7 +265,7 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
     const int lkc = (lane & 7) ^ ((lrow ^ gi) & 7);
     const bool lo = SPLIT && row >= BM;
     const int gm = min(m0 + (lo ? row - BM : row), c.M - 1);
-    asrc[i] = (lo ? c.A2 : c.A) + (size_t)gm * c.lda + lkc * 8;
+    asrc[i] = (lo ? c.A2 : c.A) + (size_t)gm * c.lda + kbase + lkc * 8;
   }
   const uint16_t* bsrc[B_INS];
 #pragma unroll
@@ -273,7 +274,7 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
     const int lkc = (lane & 7) ^ ((lrow ^ gi) & 7);
     const int vc = n0 + gi * 8 + lrow;
     const int wr = EPI == EPI_SWIGLU ? swiglu_row<WTN>(vc, c.F) : vc;
-    bsrc[i] = c.W + (size_t)wr * c.ldw + lkc * 8;
+    bsrc[i] = c.W + (size_t)wr * c.ldw + kbase + lkc * 8;
   }
 
   auto issue = [&](int kt, int stage) {
@@ -406,6 +407,12 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
   const int rowb = m0 + wm * WTM, colb = n0 + wn * WTN;
   if constexpr (EPI == EPI_RESIDUAL) epi_residual<FM, FN>(c, acc, rowb, colb, lane);
   else if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_LOGITS) epi_store<FM, FN>(c, acc, rowb, colb, lane);
+  else if constexpr (EPI == EPI_PARTIAL) {
+    GemmCall cs = c;
+    cs.outf = c.outf + (size_t)blockIdx.y * c.M * c.ldc;
+    cs.bias = nullptr;
+    epi_store<FM, FN>(cs, acc, rowb, colb, lane);
+  }
   else if constexpr (EPI == EPI_SWIGLU) epi_swiglu<FM, FN>(c, acc, rowb, colb, lane);
   else if constexpr (EPI == EPI_QKV_ROPE) epi_qkv_rope<FM, FN>(c, acc, rowb, colb, lane);
   else epi_lmstats<BM, WM, WN, FM, FN>(c, acc, m0, tn, rowb, colb, lane, wm, wn, smem);
@@ -456,21 +463,34 @@ int forced_tile() {
   return e ? std::atoi(e) : -1;
 }
 
-// Estimated time: waves of workgroups over 256 CUs, each CU running up to
-// `occ` tiles at once at its measured relative throughput.
+// Estimated seconds for a tile shape: waves of workgroups over 256 CUs, each
+// CU running up to `occ` tiles at once at its measured relative throughput
+// (a CU holding fewer tiles than it could runs proportionally less
+// efficiently), plus the fp32 partial traffic of a K split.
+double tile_time(const GemmCall& c, const TileCfg& t, int splits) {
+  const long tiles = (long)((c.M + t.BM - 1) / t.BM) * (c.N / t.BN) * splits;
+  const long slots = 256L * t.occ;
+  const long rounds = (tiles + slots - 1) / slots;
+  const long per_cu = std::min<long>(t.occ, (tiles + 255) / 256);
+  const double util = 0.5 + 0.5 * (double)per_cu / t.occ;
+  const double per_cu_flops = 6.5e12;  // ~1.7 PFLOP/s sustained over 256 CUs
+  const double tile_s = 2.0 * t.BM * t.BN * ((double)c.K / splits) / (t.eff * util * per_cu_flops);
+  const double part_s = splits > 1 ? (double)splits * c.M * c.N * 8.0 / 5.0e12 : 0.0;
+  return rounds * per_cu * tile_s + part_s;
+}
+
 int pick_tile(const GemmCall& c) {
   const int f = forced_tile();
   if (f >= 0 && f < kNumTiles && tile_ok(c, kTiles[f])) return f;
   int best = -1;
   double best_t = 0;
+  const int splits = c.epi == EPI_PARTIAL && c.splits > 1 ? c.splits : 1;
   for (int i = 0; i < kNumTiles; ++i) {
     const TileCfg& t = kTiles[i];
     if (!tile_ok(c, t)) continue;
-    const long tiles = (long)((c.M + t.BM - 1) / t.BM) * (c.N / t.BN);
-    const long slots = 256L * t.occ;
-    const long rounds = (tiles + slots - 1) / slots;
-    const long per_cu = std::min<long>(t.occ, (tiles + 255) / 256);
-    const double time = (double)rounds * per_cu * t.BM * t.BN / t.eff;
+    GemmCall full = c;
+    full.K = c.K * splits;
+    const double time = tile_time(full, t, splits);
     if (best < 0 || time < best_t) { best = i; best_t = time; }
   }
   return best;
@@ -480,7 +500,8 @@ template <int BM, int BN, int WM, int WN, int EPI>
 hipError_t launch_one(const GemmCall& c, hipStream_t st) {
   if constexpr (tile_epi(BM, BN, WM, WN, EPI)) {
     const int tiles = ((c.M + BM - 1) / BM) * (c.N / BN);
-    gemm_kernel<BM, BN, WM, WN, EPI><<<dim3(tiles), dim3(WM * WN * 64), 0, st>>>(c);
+    const int splits = EPI == EPI_PARTIAL && c.splits > 1 ? c.splits : 1;
+    gemm_kernel<BM, BN, WM, WN, EPI><<<dim3(tiles, splits), dim3(WM * WN * 64), 0, st>>>(c);
     return hipGetLastError();
   } else {
     return hipErrorInvalidValue;
@@ -495,12 +516,35 @@ hipError_t launch_cfg(const GemmCall& c, hipStream_t st) {
     case EPI_SWIGLU: return launch_one<BM, BN, WM, WN, EPI_SWIGLU>(c, st);
     case EPI_LMSTATS: return launch_one<BM, BN, WM, WN, EPI_LMSTATS>(c, st);
     case EPI_STORE_F32: return launch_one<BM, BN, WM, WN, EPI_STORE_F32>(c, st);
+    case EPI_PARTIAL: return launch_one<BM, BN, WM, WN, EPI_PARTIAL>(c, st);
     case EPI_LOGITS: return launch_one<BM, BN, WM, WN, EPI_LOGITS>(c, st);
   }
   return hipErrorInvalidValue;
 }
 
 }  // namespace
+
+int gemm_residual_splits(const GemmCall& c, int max_splits) {
+  const char* e = std::getenv("WINO_GEMM_SPLIT");
+  const int nk = c.K / BK;
+  if (e) {
+    const int s = std::atoi(e);
+    return (s >= 1 && s <= max_splits && nk % s == 0) ? s : 1;
+  }
+  double best_t = 0;
+  int best = 1;
+  for (int s = 1; s <= max_splits; ++s) {
+    if (nk % s || nk / s < 8) continue;  // keep >= 8 K steps per split
+    GemmCall p = c;
+    p.epi = s > 1 ? EPI_PARTIAL : c.epi;
+    for (int i = 0; i < kNumTiles; ++i) {
+      if (!tile_ok(p, kTiles[i])) continue;
+      const double t = tile_time(c, kTiles[i], s);
+      if (best_t == 0 || t < best_t) { best_t = t; best = s; }
+    }
+  }
+  return best;
+}
 
 int gemm_tile_n(const GemmCall& c) {
   const int i = pick_tile(c);

@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -26,11 +27,13 @@ const char* kClassNames[WINO_N_KERNEL_CLASSES] = {
     "gemm_down_residual", "select_norm", "lm_head_stats", "decide", "epilogue_stats", "gemm_logits"};
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+constexpr int kMaxSplits = 8;
 int round64(int v) { return (v + 63) / 64 * 64; }
 
 struct Layout {
-  size_t x, h, q, k, vt, att, u, hf, hf_lo, target, rope_cos, rope_sin, pm, ps, pb, pi, pt, misc, total;
+  size_t x, h, q, k, vt, att, u, hf, hf_lo, part, target, rope_cos, rope_sin, pm, ps, pb, pi, pt, misc, total;
   int max_part;
+  size_t part_elems;  // split-K partial buffer (fp32 elements)
 };
 
 Layout make_layout(const wino_model_config& c, int max_batch, int max_seq) {
@@ -51,6 +54,8 @@ Layout make_layout(const wino_model_config& c, int max_batch, int max_seq) {
   L.u = take(M * F * 2);
   L.hf = take(M * d * 2);
   L.hf_lo = take(M * d * 2);
+  L.part_elems = (size_t)kMaxSplits * std::min<size_t>(M, 1024) * d;
+  L.part = take(L.part_elems * 4);
   L.target = take(M * 4);
   L.rope_cos = take((size_t)max_seq * (hd / 2) * 4);
   L.rope_sin = take((size_t)max_seq * (hd / 2) * 4);
@@ -99,6 +104,7 @@ struct wino_ctx {
   uint16_t* u() const { return at<uint16_t>(L.u); }
   uint16_t* hf() const { return at<uint16_t>(L.hf); }
   uint16_t* hf_lo() const { return at<uint16_t>(L.hf_lo); }
+  float* part() const { return at<float>(L.part); }
   int32_t* target() const { return at<int32_t>(L.target); }
   float* rope_cos() const { return at<float>(L.rope_cos); }
   float* rope_sin() const { return at<float>(L.rope_sin); }
@@ -174,6 +180,23 @@ StepGeom make_geom(const wino_params* p, const int32_t* block_start) {
   return g;
 }
 
+// Residual-add GEMM, split over K when that fills the chip better: the fp32
+// partials land in the workspace and the caller adds them to x (fused into
+// the next RMSNorm).  Returns the number of pending partials (0 = added).
+int residual_gemm(wino_ctx* c, GemmCall g, hipStream_t st, hipError_t* err) {
+  const int cap = (int)std::min<size_t>(kMaxSplits, c->L.part_elems / ((size_t)g.M * g.N));
+  const int splits = cap > 1 ? gemm_residual_splits(g, cap) : 1;
+  if (splits > 1) {
+    g.epi = EPI_PARTIAL;
+    g.splits = splits;
+    g.K /= splits;
+    g.outf = c->part();
+    g.ldc = g.N;
+  }
+  *err = launch_gemm(g, st);
+  return splits > 1 ? splits : 0;
+}
+
 // Embedding and the first n_sub sublayers (attention and FFN halves of each
 // layer, in order); leaves the residual stream in x.
 wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, int n_sub,
@@ -181,6 +204,7 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
   const wino_model_config& m = c->cfg;
   const int d = m.d_model, F = m.d_ff, H = m.n_heads, hd = m.head_dim;
   const int M = g.B * g.T;
+  int pend = 0;  // split-K partials not yet added to x
   {
     Bracket br(c, K_EMBED_NORM, st);
     launch_embed_norm(g, tokens, c->tok_emb, m.vocab, c->attn_norm[0], m.rms_eps, d, c->x(), c->h(), st);
@@ -209,15 +233,18 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
     oc.M = M; oc.N = d; oc.K = d; oc.epi = EPI_RESIDUAL; oc.outf = c->x(); oc.ldc = d;
     {
       Bracket br(c, K_GEMM_O, st);
-      HIP_TRY(c, launch_gemm(oc, st));
+      hipError_t e;
+      pend = residual_gemm(c, oc, st, &e);
+      HIP_TRY(c, e);
       br.done(2.0 * M * d * d, 2.0 * ((double)M * d + (double)d * d) + 8.0 * M * d);
     }
     if (2 * l + 1 >= n_sub) break;
     {
       Bracket br(c, K_RMSNORM, st);
-      launch_rmsnorm(c->x(), c->ffn_norm[l], m.rms_eps, M, d, c->h(), st);
+      launch_rmsnorm(c->x(), c->ffn_norm[l], m.rms_eps, M, d, c->h(), pend ? c->part() : nullptr, pend, st);
       HIP_TRY(c, hipGetLastError());
-      br.done(0, (double)M * d * 6);
+      br.done(0, (double)M * d * (6 + 8 * (pend ? 1 : 0)) + 4.0 * M * d * pend);
+      pend = 0;
     }
     GemmCall gc{};
     gc.A = c->h(); gc.lda = d; gc.W = c->w_gu[l]; gc.ldw = d;
@@ -232,15 +259,25 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
     dc.M = M; dc.N = d; dc.K = F; dc.epi = EPI_RESIDUAL; dc.outf = c->x(); dc.ldc = d;
     {
       Bracket br(c, K_GEMM_DOWN, st);
-      HIP_TRY(c, launch_gemm(dc, st));
+      hipError_t e;
+      pend = residual_gemm(c, dc, st, &e);
+      HIP_TRY(c, e);
       br.done(2.0 * M * (double)F * d, 2.0 * ((double)M * F + (double)F * d) + 8.0 * M * d);
     }
     if (l + 1 < m.n_layers && 2 * (l + 1) < n_sub) {
       Bracket br(c, K_RMSNORM, st);
-      launch_rmsnorm(c->x(), c->attn_norm[l + 1], m.rms_eps, M, d, c->h(), st);
+      launch_rmsnorm(c->x(), c->attn_norm[l + 1], m.rms_eps, M, d, c->h(), pend ? c->part() : nullptr,
+                     pend, st);
       HIP_TRY(c, hipGetLastError());
-      br.done(0, (double)M * d * 6);
+      br.done(0, (double)M * d * (6 + 8 * (pend ? 1 : 0)) + 4.0 * M * d * pend);
+      pend = 0;
     }
+  }
+  if (pend) {
+    Bracket br(c, K_RMSNORM, st);
+    launch_residual_reduce(c->x(), c->part(), pend, M, d, st);
+    HIP_TRY(c, hipGetLastError());
+    br.done(0, (double)M * d * 8 + 4.0 * M * d * pend);
   }
   return WINO_OK;
 }
