@@ -8,12 +8,18 @@
 // Layout: q, k bf16 [B, H, Tp, hd] (RoPE already applied), v transposed
 // [B, H, hd, Tp]; output o bf16 [B*T, H*hd] row-major.
 //
-// Each wave owns 32 query rows.  Scores are computed transposed, S^T = K Q^T,
-// so after the 32x32x16 MFMA a lane holds 32 keys of ONE query row: the
-// online-softmax max / sum stay inside the lane (plus its partner lane 32
-// apart).  The same registers, split into hi and lo bf16 parts, are the B
-// operand of O^T = V^T P^T, whose A operand comes from the transposed V tile
-// in LDS; the per-lane key order of P and V^T is matched slot by slot.
+// Each wave owns 32 query rows.  Scores are computed transposed, S^T = K Q^T
+// (32x32x16 MFMA), so a lane holds 32 keys of ONE query row and the online
+// softmax max / sum stay inside the lane (plus its partner lane 32 apart).
+// The same registers, split into hi and lo bf16 parts, are the B operand of
+// O^T = V^T P^T.
+//
+// K and V^T tiles of 64 keys stream global -> LDS by LDS-DMA into two stages
+// (the next tile loads while the current one is used), with 16-byte chunks
+// XOR-swizzled per row so fragment reads are free of bank conflicts.  Within
+// each 32-key block the K rows are stored in a permuted key order (bits 2 and
+// 3 of the key index swapped): the MFMA then leaves each lane's P values for
+// 8 CONSECUTIVE keys of a 16-key step, so its V^T operand is one 16-byte read.
 #include "common.h"
 #include "kernels.h"
 
@@ -22,18 +28,31 @@ namespace {
 
 constexpr int BKV = 64;
 
+// key (within a 32-key block) held by MFMA output register i of lane group g
+__device__ __forceinline__ int key_of(int i, int g) {
+  const int ih = i >> 2;
+  return 16 * (ih >> 1) + 8 * g + 4 * (ih & 1) + (i & 3);
+}
+// LDS row r of a K tile holds key perm(r): bits 2 and 3 swapped within 32
+__device__ __forceinline__ int perm_key(int r) {
+  return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
+}
+
 template <int HD, int NW>
 __global__ __launch_bounds__(NW * 64) void attn_kernel(StepGeom g, const uint16_t* __restrict__ q,
                                                        const uint16_t* __restrict__ k,
                                                        const uint16_t* __restrict__ vt, int H,
                                                        uint16_t* __restrict__ o, float scale_log2) {
-  constexpr int LDKS = HD + 8;  // K tile row stride (bf16), 16-byte padded
-  constexpr int LDV = BKV + 8;  // V^T tile row stride
-  constexpr int FE = HD / 32;   // 32-wide output blocks over the head dim
-  constexpr int KS = HD / 16;   // 16-deep k steps over the head dim
-  constexpr int NT = NW * 64;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[BKV * LDKS];
-  __shared__ __attribute__((aligned(16))) uint16_t Vs[HD * LDV];
+  constexpr int FE = HD / 32;        // 32-wide output blocks over the head dim
+  constexpr int KS = HD / 16;        // 16-deep k steps over the head dim
+  constexpr int KCH = HD / 8;        // 16-byte chunks per K row
+  constexpr int KROWS = 1024 / (2 * HD);  // K rows per 1 KB DMA instruction
+  constexpr int K_INS = BKV / KROWS / NW;  // K DMA instructions per wave
+  constexpr int V_INS = HD / 8 / NW;       // V^T DMA instructions per wave (8 rows each)
+  static_assert(K_INS * KROWS * NW == BKV && V_INS * 8 * NW == HD, "loader split");
+  constexpr int KTILE = BKV * HD;    // bf16 elements
+  constexpr int STAGE = 2 * KTILE;   // K tile then V^T tile
+  __shared__ __attribute__((aligned(1024))) uint16_t smem[2 * STAGE];
 
   const int b = blockIdx.z, h = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, grp = lane >> 5;
@@ -47,6 +66,44 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(StepGeom g, const uint16_
   const uint16_t* qb = q + bh * g.Tp * HD;
   const uint16_t* kb = k + bh * g.Tp * HD;
   const uint16_t* vb = vt + bh * HD * g.Tp;
+
+  // DMA sources (per lane, fixed offsets; the key tile start is added later)
+  int koff[K_INS];   // element offset of this lane's 16 bytes for K row r, relative to key 0
+  int krow[K_INS];   // tile-relative key of that row
+#pragma unroll
+  for (int i = 0; i < K_INS; ++i) {
+    const int gi = wave * K_INS + i;
+    const int r = gi * KROWS + lane / (KCH);
+    const int pos = lane % KCH;
+    const int swz = KCH == 16 ? (r & 15) : ((r ^ (r >> 3)) & 7);
+    krow[i] = (r & ~31) | perm_key(r & 31);
+    koff[i] = (pos ^ swz) * 8;
+  }
+  const uint16_t* vsrc[V_INS];
+#pragma unroll
+  for (int i = 0; i < V_INS; ++i) {
+    const int gi = wave * V_INS + i;
+    const int e = gi * 8 + (lane >> 3);
+    const int pos = lane & 7;
+    vsrc[i] = vb + (size_t)e * g.Tp + (pos ^ ((e ^ (e >> 3)) & 7)) * 8;
+  }
+  auto issue = [&](int kv0, int stage) {
+    uint16_t* sK = smem + stage * STAGE;
+    uint16_t* sV = sK + KTILE;
+#pragma unroll
+    for (int i = 0; i < K_INS; ++i) {
+      const int key = min(kv0 + krow[i], g.T - 1);  // keys >= T are masked below
+      __builtin_amdgcn_global_load_lds((const void*)(kb + (size_t)key * HD + koff[i]),
+                                       (__attribute__((address_space(3))) void*)(sK + (wave * K_INS + i) * 512),
+                                       16, 0, 0);
+    }
+    // Tp is a multiple of 64: the whole V^T tile row lies inside the buffer
+#pragma unroll
+    for (int i = 0; i < V_INS; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(vsrc[i] + kv0),
+                                       (__attribute__((address_space(3))) void*)(sV + (wave * V_INS + i) * 512),
+                                       16, 0, 0);
+  };
 
   bf16x8 qf[KS];
   {
@@ -64,25 +121,35 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(StepGeom g, const uint16_
   float mrun = kNegBig, lrun = 0.f;
 
   const int q_last = min(q0 + NW * 32, g.T) - 1;
-  const int kend = q_last >= g.S ? g.T : g.S;  // shadow rows also see keys S..T-1
+  const bool has_shadow = q_last >= g.S;
+  const int kend = has_shadow ? g.T : g.S;  // shadow rows also see keys S..T-1
+  const int ntile = (kend + BKV - 1) / BKV;
 
-  for (int kv0 = 0; kv0 < kend; kv0 += BKV) {
+  // fragment-read swizzles of the rows this lane reads (fixed over tiles)
+  const int kr = lane & 31;                    // K rows kb2*32 + kr
+  int kswz[2];
+#pragma unroll
+  for (int kb2 = 0; kb2 < 2; ++kb2) {
+    const int r = kb2 * 32 + kr;
+    kswz[kb2] = KCH == 16 ? (r & 15) : ((r ^ (r >> 3)) & 7);
+  }
+  int vswz[FE];
+#pragma unroll
+  for (int fe = 0; fe < FE; ++fe) {
+    const int e = fe * 32 + (lane & 31);
+    vswz[fe] = (e ^ (e >> 3)) & 7;
+  }
+
+  issue(0, 0);
+  for (int t = 0; t < ntile; ++t) {
+    const int kv0 = t * BKV;
+    // own copies of tile t landed; after the barrier everyone's have, and
+    // everyone finished tile t-1, whose stage tile t+1 may now overwrite
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    for (int ci = tid; ci < BKV * HD / 8; ci += NT) {
-      const int r = ci / (HD / 8), cc = ci - r * (HD / 8);
-      const int key = kv0 + r;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (key < g.T) v = *reinterpret_cast<const uint4*>(kb + (size_t)key * HD + cc * 8);
-      *reinterpret_cast<uint4*>(Ks + r * LDKS + cc * 8) = v;
-    }
-    for (int ci = tid; ci < HD * BKV / 8; ci += NT) {
-      const int e = ci / (BKV / 8), cc = ci - e * (BKV / 8);
-      // Tp is a multiple of 64, so the whole tile row is inside the buffer;
-      // columns >= T get probability 0 below.
-      const uint4 v = *reinterpret_cast<const uint4*>(vb + (size_t)e * g.Tp + kv0 + cc * 8);
-      *reinterpret_cast<uint4*>(Vs + e * LDV + cc * 8) = v;
-    }
-    __syncthreads();
+    if (t + 1 < ntile) issue(kv0 + BKV, (t + 1) & 1);
+    const uint16_t* sK = smem + (t & 1) * STAGE;
+    const uint16_t* sV = sK + KTILE;
 
     f32x16 s[2];
 #pragma unroll
@@ -91,32 +158,43 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(StepGeom g, const uint16_
       for (int i = 0; i < 16; ++i) s[kb2][i] = 0.f;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
+        const int ch = (ks * 2 + grp) ^ kswz[kb2];
         const bf16x8 kf = as_bf16x8(
-            *reinterpret_cast<const uint4*>(Ks + (kb2 * 32 + (lane & 31)) * LDKS + ks * 16 + grp * 8));
+            *reinterpret_cast<const uint4*>(sK + (kb2 * 32 + kr) * HD + ch * 8));
         s[kb2] = mfma32(kf, qf[ks], s[kb2]);
       }
     }
 
+    // Only tiles that reach past S or hold an excluded shadow column need the
+    // mask predicate; the test is uniform over the workgroup.
+    const bool edge = kv0 + BKV > g.S || (has_shadow && kv0 < c0 + g.Lb && kv0 + BKV > c0);
     float tmax = kNegBig;
+    if (edge) {
+#pragma unroll
+      for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = kv0 + kb2 * 32 + key_of(i, grp);
+          const bool ok = key < klim && key != excl;
+          s[kb2][i] = ok ? s[kb2][i] : kNegBig;
+        }
+    }
 #pragma unroll
     for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int key = kv0 + kb2 * 32 + mfma_row(i, lane);
-        const bool ok = key < klim && key != excl;
-        const float v = ok ? s[kb2][i] * scale_log2 : kNegBig;
-        s[kb2][i] = v;
-        tmax = fmaxf(tmax, v);
-      }
+      for (int i = 0; i < 16; ++i) tmax = fmaxf(tmax, s[kb2][i]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    // running max in raw score units; probabilities exp2(s*c - m*c) with
+    // c = log2(e)/sqrt(hd): one FMA per score
     const float mnew = fmaxf(mrun, tmax);
-    const float alpha = exp2f(mrun - mnew);
+    const float alpha = exp2f((mrun - mnew) * scale_log2);
+    const float mc = mnew == kNegBig ? 0.f : mnew * scale_log2;
     float psum = 0.f;
 #pragma unroll
     for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float p = s[kb2][i] == kNegBig ? 0.f : exp2f(s[kb2][i] - mnew);
+        const float p = exp2f(fmaf(s[kb2][i], scale_log2, -mc));
         s[kb2][i] = p;
         psum += p;
       }
@@ -130,7 +208,8 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(StepGeom g, const uint16_
 #pragma unroll
     for (int ks4 = 0; ks4 < BKV / 16; ++ks4) {
       // P as hi + lo bf16 parts: the product with V keeps ~16 mantissa bits
-      // of the probabilities instead of bf16's 8
+      // of the probabilities instead of bf16's 8.  Registers 8*(ks4&1)..+7 of
+      // block ks4/2 hold keys 16*ks4 + 8*grp + 0..7.
       const int base = 8 * (ks4 & 1);
       uint32_t ph[4], pl[4];
 #pragma unroll
@@ -143,10 +222,9 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(StepGeom g, const uint16_
       const bf16x8 pf_lo = as_bf16x8(make_uint4(pl[0], pl[1], pl[2], pl[3]));
 #pragma unroll
       for (int fe = 0; fe < FE; ++fe) {
-        const uint16_t* vr = Vs + (fe * 32 + (lane & 31)) * LDV + 16 * ks4 + 4 * grp;
-        const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vr + 8);
-        const bf16x8 vf = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+        const int row = fe * 32 + (lane & 31);
+        const int ch = (ks4 * 2 + grp) ^ vswz[fe];
+        const bf16x8 vf = as_bf16x8(*reinterpret_cast<const uint4*>(sV + row * BKV + ch * 8));
         oacc[fe] = mfma32(vf, pf_hi, oacc[fe]);
         oacc[fe] = mfma32(vf, pf_lo, oacc[fe]);
       }
@@ -160,24 +238,40 @@ __global__ __launch_bounds__(NW * 64) void attn_kernel(StepGeom g, const uint16_
 #pragma unroll
     for (int fe = 0; fe < FE; ++fe)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) dst[fe * 32 + mfma_row(i, lane)] = f2bf(oacc[fe][i] * inv);
+      for (int i = 0; i < 16; i += 4) {
+        // rows 8*(i/4) + 4*grp + 0..3 of this e block: 4 consecutive outputs
+        uint2 w;
+        w.x = pack2bf(oacc[fe][i] * inv, oacc[fe][i + 1] * inv);
+        w.y = pack2bf(oacc[fe][i + 2] * inv, oacc[fe][i + 3] * inv);
+        *reinterpret_cast<uint2*>(dst + fe * 32 + mfma_row(i, lane)) = w;
+      }
   }
+}
+
+template <int HD>
+hipError_t launch_hd(const StepGeom& g, const uint16_t* q, const uint16_t* k, const uint16_t* vt,
+                     int H, uint16_t* o, float scale_log2, hipStream_t st) {
+  // 128-query workgroups when there are enough of them to fill the chip,
+  // otherwise 64-query ones (more workgroups per head).
+  const long wg128 = (long)((g.T + 127) / 128) * H * g.B;
+  if (wg128 >= 512) {
+    dim3 grid((g.T + 127) / 128, H, g.B);
+    attn_kernel<HD, 4><<<grid, 256, 0, st>>>(g, q, k, vt, H, o, scale_log2);
+  } else {
+    dim3 grid((g.T + 63) / 64, H, g.B);
+    attn_kernel<HD, 2><<<grid, 128, 0, st>>>(g, q, k, vt, H, o, scale_log2);
+  }
+  return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_attention(const StepGeom& g, const uint16_t* q, const uint16_t* k,
                             const uint16_t* vt, int H, int hd, uint16_t* o, hipStream_t st) {
-  constexpr int NW = 4;
-  dim3 grid((g.T + NW * 32 - 1) / (NW * 32), H, g.B), block(NW * 64);
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
-  if (hd == 128)
-    attn_kernel<128, NW><<<grid, block, 0, st>>>(g, q, k, vt, H, o, scale_log2);
-  else if (hd == 64)
-    attn_kernel<64, NW><<<grid, block, 0, st>>>(g, q, k, vt, H, o, scale_log2);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+  if (hd == 128) return launch_hd<128>(g, q, k, vt, H, o, scale_log2, st);
+  if (hd == 64) return launch_hd<64>(g, q, k, vt, H, o, scale_log2, st);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace wino
