@@ -39,7 +39,7 @@ __device__ __forceinline__ int perm_key(int r) {
 }
 
 template <int HD, int NW>
-__global__ __launch_bounds__(NW * 64) void attn_kernel(StepGeom g, const uint16_t* __restrict__ q,
+__global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const uint16_t* __restrict__ q,
                                                        const uint16_t* __restrict__ k,
                                                        const uint16_t* __restrict__ vt, int H,
                                                        uint16_t* __restrict__ o, float scale_log2) {
