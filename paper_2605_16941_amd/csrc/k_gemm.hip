@@ -97,45 +97,122 @@ __device__ __forceinline__ void epi_swiglu(const GemmCall& c, f32x16 (&acc)[FM][
 }
 
 // Wave columns = one head (WTN == hd): lane holds columns e and e + hd/2 of
-// the rotate-half pair in fragments fn and fn + FN/2.
+// the rotate-half pair in fragments fn and fn + FN/2.  The wave's rotated q/k
+// rows (or its v columns, transposed) are staged in the wave's own LDS region
+// of WTM x hd bf16 and leave in 16-byte stores: whole q/k rows of hd elements,
+// and runs of 8 consecutive positions of v^T.  Storing v^T straight from the
+// MFMA layout would scatter 2-byte writes over hd rows of the transposed
+// buffer.  16-byte chunks are XOR-swizzled by the row index, so the
+// half-waves' writes (4 rows apart) land in distinct banks.
 template <int FM, int FN>
 __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM][FN], int rowb,
-                                             int colb, int lane) {
+                                             int colb, int lane, uint16_t* ws) {
   constexpr int H2 = FN / 2;
+  constexpr int WTM = FM * 32, HD = FN * 32;
+  constexpr int QCH = HD / 8;   // 16-byte chunks per q/k row (power of two)
+  constexpr int VCH = WTM / 8;  // 16-byte chunks per v^T row
+  // v^T rows are 2*VCH slots of 8 bytes; slot s of row e sits at s ^ m(e),
+  // m(e) = (e >> 1) & SMASK, so 32 consecutive rows written at one slot
+  // cover 64 distinct banks.  A 16-byte chunk stays whole (its halves swap
+  // when m(e) is odd).
+  constexpr int SL = 2 * VCH;
+  constexpr int SMASK = SL % 16 == 0 ? 15 : SL % 8 == 0 ? 7 : SL % 4 == 0 ? 3 : 1;
+  static_assert((QCH & (QCH - 1)) == 0 && 64 % QCH == 0, "q/k chunking");
+  static_assert((HD * VCH) % 64 == 0, "v^T chunking");
   const RopeOut& ro = c.rope;
   const StepGeom& g = c.geom;
-  const int hd = ro.hd, half = hd / 2;
-  const int d = ro.H * hd;
+  const int half = HD / 2;
+  const int d = ro.H * HD;
   const int which = colb / d;               // 0 q, 1 k, 2 v
-  const int head = (colb - which * d) / hd;
+  const int head = (colb - which * d) / HD;
+  if (which < 2) {
 #pragma unroll
-  for (int fm = 0; fm < FM; ++fm)
+    for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int row = rowb + fm * 32 + mfma_row(i, lane);
-      if (row >= c.M) continue;
-      const int b = row / g.T, t = row - b * g.T;
-      const size_t bh = (size_t)b * ro.H + head;
-      if (which < 2) {
+      for (int i = 0; i < 16; ++i) {
+        const int lr = fm * 32 + mfma_row(i, lane);
+        const int row = rowb + lr;
+        if (row >= c.M) continue;
+        const int b = row / g.T, t = row - b * g.T;
         const int pos = row_pos(g, b, t);
-        uint16_t* dst = (which == 0 ? ro.q : ro.k) + (bh * g.Tp + t) * hd;
+        uint16_t* wr = ws + lr * HD;
+        const int sw = lr & (QCH - 1);
 #pragma unroll
         for (int fn = 0; fn < H2; ++fn) {
           const int e = fn * 32 + (lane & 31);
           const float cs = ro.cos_t[(size_t)pos * half + e], sn = ro.sin_t[(size_t)pos * half + e];
           const float x1 = acc[fm][fn][i], x2 = acc[fm][fn + H2][i];
-          dst[e] = f2bf(x1 * cs - x2 * sn);
-          dst[e + half] = f2bf(x2 * cs + x1 * sn);
+          const float r1 = x1 * cs - x2 * sn;  // element e
+          const float r2 = x2 * cs + x1 * sn;  // element e + hd/2
+          // lane pairs trade one value: the even lane stores elements e, e+1,
+          // the odd lane elements e+hd/2-1, e+hd/2 (one 4-byte write each)
+          const bool odd = lane & 1;
+          const float got = __shfl_xor(odd ? r1 : r2, 1, 64);
+          const int ee = odd ? e + half - 1 : e;
+          const uint32_t pk = odd ? pack2bf(got, r2) : pack2bf(r1, got);
+          *reinterpret_cast<uint32_t*>(wr + (((ee >> 3) ^ sw) << 3) + (ee & 7)) = pk;
         }
-      } else {
-        uint16_t* dst = ro.vt + bh * hd * g.Tp + t;
+      }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    uint16_t* base = which == 0 ? ro.q : ro.k;
+    constexpr int RPI = 64 / QCH;  // rows per pass
 #pragma unroll
-        for (int fn = 0; fn < FN; ++fn) {
-          const int e = fn * 32 + (lane & 31);
-          dst[(size_t)e * g.Tp] = f2bf(acc[fm][fn][i]);
+    for (int it = 0; it < WTM / RPI; ++it) {
+      const int lr = it * RPI + lane / QCH, ch = lane & (QCH - 1);
+      const int row = rowb + lr;
+      if (row >= c.M) continue;
+      const int b = row / g.T, t = row - b * g.T;
+      const size_t bh = (size_t)b * ro.H + head;
+      const uint4 v = *reinterpret_cast<const uint4*>(ws + lr * HD + ((ch ^ (lr & (QCH - 1))) << 3));
+      *reinterpret_cast<uint4*>(base + (bh * g.Tp + t) * HD + ch * 8) = v;
+    }
+  } else {
+    // v^T staging: LDS row e holds the WTM positions of this wave; lane writes
+    // the 4 consecutive positions 8*(i/4) + 4*(lane/32) + 0..3 of fragment fm.
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) {
+      const int e = fn * 32 + (lane & 31);
+      uint16_t* wr = ws + e * WTM;
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int tl = fm * 32 + 8 * q + 4 * (lane >> 5);
+          uint2 v;
+          v.x = pack2bf(acc[fm][fn][4 * q], acc[fm][fn][4 * q + 1]);
+          v.y = pack2bf(acc[fm][fn][4 * q + 2], acc[fm][fn][4 * q + 3]);
+          const int slot = (tl >> 2) ^ ((e >> 1) & SMASK);
+          *reinterpret_cast<uint2*>(wr + slot * 4) = v;
+        }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+    for (int it = 0; it < HD * VCH / 64; ++it) {
+      const int idx = it * 64 + lane;
+      const int e = idx / VCH, ch = idx - (idx / VCH) * VCH;
+      const int m = (e >> 1) & SMASK;
+      uint4 v = *reinterpret_cast<const uint4*>(ws + e * WTM + ((ch ^ (m >> 1)) << 3));
+      if (m & 1) v = make_uint4(v.z, v.w, v.x, v.y);
+      const int r0 = rowb + ch * 8;
+      if (r0 >= c.M) continue;
+      const int b = r0 / g.T, t0 = r0 - b * g.T;
+      if (r0 + 7 < c.M && t0 + 7 < g.T && (t0 & 7) == 0) {
+        const size_t bh = (size_t)b * ro.H + head;
+        *reinterpret_cast<uint4*>(ro.vt + (bh * HD + e) * g.Tp + t0) = v;
+      } else {
+        // run crosses a sequence end or the last row, or T is not a multiple
+        // of 8: element stores
+        const uint16_t* h = reinterpret_cast<const uint16_t*>(&v);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int r = r0 + j;
+          if (r >= c.M) break;
+          const int bj = r / g.T, tj = r - bj * g.T;
+          ro.vt[(((size_t)bj * ro.H + head) * HD + e) * g.Tp + tj] = h[j];
         }
       }
     }
+  }
 }
 
 // LM head epilogue: per row of the tile, statistics over the BN columns.
@@ -414,7 +491,11 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
     epi_store<FM, FN>(cs, acc, rowb, colb, lane);
   }
   else if constexpr (EPI == EPI_SWIGLU) epi_swiglu<FM, FN>(c, acc, rowb, colb, lane);
-  else if constexpr (EPI == EPI_QKV_ROPE) epi_qkv_rope<FM, FN>(c, acc, rowb, colb, lane);
+  else if constexpr (EPI == EPI_QKV_ROPE) {
+    // each wave stages its WTM x WTN tile in its own LDS region
+    static_assert(BM * BN <= 2 * STAGE, "QKV staging fits the pipeline LDS");
+    epi_qkv_rope<FM, FN>(c, acc, rowb, colb, lane, smem + wave * (WTM * WTN));
+  }
   else epi_lmstats<BM, WM, WN, FM, FN>(c, acc, m0, tn, rowb, colb, lane, wm, wn, smem);
 }
 
