@@ -20,8 +20,11 @@
 // (BM/WM) x (BN/WN) sub-tile of 32x32 MFMA blocks.  Workgroups are renumbered
 // so that each XCD works on one contiguous range of tiles (shared W tiles stay
 // in that XCD's L2).
+#include <algorithm>
 #include <climits>
+#include <cmath>
 #include <cstdlib>
+#include <mutex>
 
 #include "common.h"
 #include "kernels.h"
@@ -73,6 +76,24 @@ __device__ __forceinline__ void epi_store(const GemmCall& c, f32x16 (&acc)[FM][F
       float* dst = c.outf + (size_t)row * c.ldc + colb + (lane & 31);
 #pragma unroll
       for (int fn = 0; fn < FN; ++fn) dst[fn * 32] = acc[fm][fn][i] + bias[fn];
+    }
+}
+
+// K-slice `split` of a tile above split_row0: fp32 partial
+// part[split][m - split_row0][n] (row stride N), summed into x later.
+template <int FM, int FN>
+__device__ __forceinline__ void epi_partial(const GemmCall& c, f32x16 (&acc)[FM][FN], int rowb,
+                                            int colb, int lane, int split) {
+  const size_t mt = (size_t)(c.M - c.split_row0);
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int row = rowb + fm * 32 + mfma_row(i, lane);
+      if (row >= c.M) continue;
+      float* dst = c.part + (split * mt + (row - c.split_row0)) * c.N + colb + (lane & 31);
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) dst[fn * 32] = acc[fm][fn][i];
     }
 }
 
@@ -316,13 +337,26 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
   // Tile order: each XCD takes a contiguous range of logical tiles, walked in
   // groups of GM M-tiles so the ~32 workgroups an XCD runs at once cover
   // GM A tiles x (32/GM) W tiles and reuse both from its L2.
+  // Work units: whole-K tiles of the rows below split_row0 first, then (the
+  // residual epilogue only) `splits` K-slices of each tile above it, so a
+  // last partial round of whole tiles becomes a full round of thin slices.
   constexpr int GM = 8;
   const int nTM = (c.M + BM - 1) / BM, nTN = c.N / BN;
-  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  const bool has_tail = EPI == EPI_RESIDUAL && c.splits > 1;
+  const int mainTM = has_tail ? c.split_row0 / BM : nTM;
+  const int n_main = mainTM * nTN;
+  const bool tail = (int)blockIdx.x >= n_main;
+  const int tailTM = nTM - mainTM;
+  const int u = tail ? xcd_remap(blockIdx.x - n_main, gridDim.x - n_main)
+                     : xcd_remap(blockIdx.x, n_main);
+  const int split = tail ? u / (tailTM * nTN) : 0;
+  const int t = tail ? u - split * (tailTM * nTN) : u;
+  const int rTM = tail ? tailTM : mainTM;
   const int first_m = (t / (GM * nTN)) * GM;
-  const int gsz = min(nTM - first_m, GM);
-  const int tm = first_m + (t % (GM * nTN)) % gsz;
+  const int gsz = min(rTM - first_m, GM);
+  const int tm = (tail ? mainTM : 0) + first_m + (t % (GM * nTN)) % gsz;
   const int tn = (t % (GM * nTN)) / gsz;
+  const int Ku = tail ? c.K / c.splits : c.K;  // K depth of this unit
   const int m0 = tm * BM, n0 = tn * BN;
 
   // Tile rows are 128 bytes = 8 chunks of 16 bytes; chunk kc of row r is
@@ -333,7 +367,7 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
   // The lane that fills position (lane & 7) of row 8*i + lane/8 of a tile
   // therefore fetches chunk (lane & 7) ^ ((lane/8 ^ i) & 7).
   const int lrow = lane >> 3;
-  const int kbase = blockIdx.y * c.K;  // split-K: this split's first column
+  const int kbase = split * Ku;  // first K column of this unit
   const uint16_t* asrc[A_INS];
 #pragma unroll
   for (int i = 0; i < A_INS; ++i) {
@@ -377,7 +411,7 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[fm][fn][i] = 0.f;
 
-  const int nk = c.K / BK;
+  const int nk = Ku / BK;
   const int arow = wm * WTM + (lane & 31), brow = wn * WTN + (lane & 31);
   // swizzle of each fragment row this lane reads (fixed over the K loop)
   int aswz[FM], alswz[SPLIT ? FM : 1], bswz[FN];
@@ -482,14 +516,11 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
   __syncthreads();
 
   const int rowb = m0 + wm * WTM, colb = n0 + wn * WTN;
-  if constexpr (EPI == EPI_RESIDUAL) epi_residual<FM, FN>(c, acc, rowb, colb, lane);
-  else if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_LOGITS) epi_store<FM, FN>(c, acc, rowb, colb, lane);
-  else if constexpr (EPI == EPI_PARTIAL) {
-    GemmCall cs = c;
-    cs.outf = c.outf + (size_t)blockIdx.y * c.M * c.ldc;
-    cs.bias = nullptr;
-    epi_store<FM, FN>(cs, acc, rowb, colb, lane);
+  if constexpr (EPI == EPI_RESIDUAL) {
+    if (!tail) epi_residual<FM, FN>(c, acc, rowb, colb, lane);
+    else epi_partial<FM, FN>(c, acc, rowb, colb, lane, split);
   }
+  else if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_LOGITS) epi_store<FM, FN>(c, acc, rowb, colb, lane);
   else if constexpr (EPI == EPI_SWIGLU) epi_swiglu<FM, FN>(c, acc, rowb, colb, lane);
   else if constexpr (EPI == EPI_QKV_ROPE) {
     // each wave stages its WTM x WTN tile in its own LDS region
@@ -539,50 +570,97 @@ bool tile_ok(const GemmCall& c, const TileCfg& t) {
   return true;
 }
 
-int forced_tile() {
-  const char* e = std::getenv("WINO_GEMM_TILE");
-  return e ? std::atoi(e) : -1;
+int env_int(const char* name, int dflt) {
+  const char* e = std::getenv(name);
+  return e ? std::atoi(e) : dflt;
 }
 
-// Estimated seconds for a tile shape: waves of workgroups over 256 CUs, each
-// CU running up to `occ` tiles at once at its measured relative throughput
-// (a CU holding fewer tiles than it could runs proportionally less
-// efficiently), plus the fp32 partial traffic of a K split.
-double tile_time(const GemmCall& c, const TileCfg& t, int splits) {
-  const long tiles = (long)((c.M + t.BM - 1) / t.BM) * (c.N / t.BN) * splits;
+// Throughput model: a CU sustains ~6.5 TFLOP/s of bf16 MFMA (~1.7 PFLOP/s
+// over 256 CUs) times the tile's relative efficiency, shared by the `occ`
+// workgroups it holds; epilogue traffic moves at ~4 TB/s shared by all slots.
+constexpr double kCuFlops = 6.5e12, kEpiBw = 4.0e12, kPartBw = 2.5e12;
+
+// Estimated seconds for whole-K tiles: waves of workgroups over 256 CUs (a CU
+// holding fewer tiles than it could runs proportionally less efficiently).
+double tile_time(const GemmCall& c, const TileCfg& t) {
+  const long tiles = (long)((c.M + t.BM - 1) / t.BM) * (c.N / t.BN);
   const long slots = 256L * t.occ;
   const long rounds = (tiles + slots - 1) / slots;
   const long per_cu = std::min<long>(t.occ, (tiles + 255) / 256);
   const double util = 0.5 + 0.5 * (double)per_cu / t.occ;
-  const double per_cu_flops = 6.5e12;  // ~1.7 PFLOP/s sustained over 256 CUs
-  const double tile_s = 2.0 * t.BM * t.BN * ((double)c.K / splits) / (t.eff * util * per_cu_flops);
-  const double part_s = splits > 1 ? (double)splits * c.M * c.N * 8.0 / 5.0e12 : 0.0;
-  return rounds * per_cu * tile_s + part_s;
+  const double tile_s = 2.0 * t.BM * t.BN * (double)c.K / (t.eff * util * kCuFlops);
+  return rounds * per_cu * tile_s;
+}
+
+// Makespan of n_main jobs of length T followed by n_units jobs of length U,
+// each started on the slot that frees first (the hardware dispatcher's order).
+double makespan(long n_main, double T, long n_units, double U, long slots) {
+  const long R = n_main / slots, r = n_main % slots;
+  const double main_end = (R + (r ? 1 : 0)) * T;
+  if (n_units == 0) return main_end;
+  const long early = slots - r;  // slots free at R*T; the other r at (R+1)*T
+  double best = 0;
+  for (long j = 1;; ++j) {
+    const double X = R * T + j * U;
+    const long late = r ? (long)std::floor(std::max(0.0, (X - (R + 1) * T) / U) + 1e-9) : 0;
+    if (early * j + r * late >= n_units) { best = X; break; }
+  }
+  if (r) {
+    for (long j = 1;; ++j) {
+      const double X = (R + 1) * T + j * U;
+      if (X >= best) break;
+      const long e = (long)std::floor((X - R * T) / U + 1e-9);
+      if (early * e + r * j >= n_units) { best = X; break; }
+    }
+  }
+  return std::max(main_end, best);
+}
+
+// Residual GEMM: whole-K tiles read-add-write 8 bytes of x per output; the
+// `splits` K-slices of the last tail_tm row tiles write 4-byte partials that
+// the next norm kernel reads back.
+double residual_time(const GemmCall& c, const TileCfg& t, int tail_tm, int splits) {
+  const int nTM = (c.M + t.BM - 1) / t.BM, nTN = c.N / t.BN;
+  const long slots = 256L * t.occ;
+  const double rate = t.eff * kCuFlops / t.occ;
+  const double out_s = (double)t.BM * t.BN / (kEpiBw / slots);
+  const double T = 2.0 * t.BM * t.BN * (double)c.K / rate + 8.0 * out_s;
+  const long n_main = (long)(nTM - tail_tm) * nTN;
+  if (tail_tm == 0) return makespan(n_main, T, 0, 0, slots);
+  const double U = 2.0 * t.BM * t.BN * ((double)c.K / splits + 2 * BK) / rate + 4.0 * out_s;
+  const long n_units = (long)tail_tm * nTN * splits;
+  const double tail_rows = c.M - (double)(nTM - tail_tm) * t.BM;
+  return makespan(n_main, T, n_units, U, slots) + splits * tail_rows * c.N * 4.0 / kPartBw;
 }
 
 int pick_tile(const GemmCall& c) {
-  const int f = forced_tile();
+  const int f = env_int("WINO_GEMM_TILE", -1);
   if (f >= 0 && f < kNumTiles && tile_ok(c, kTiles[f])) return f;
   int best = -1;
   double best_t = 0;
-  const int splits = c.epi == EPI_PARTIAL && c.splits > 1 ? c.splits : 1;
   for (int i = 0; i < kNumTiles; ++i) {
-    const TileCfg& t = kTiles[i];
-    if (!tile_ok(c, t)) continue;
-    GemmCall full = c;
-    full.K = c.K * splits;
-    const double time = tile_time(full, t, splits);
+    if (!tile_ok(c, kTiles[i])) continue;
+    const double time = tile_time(c, kTiles[i]);
     if (best < 0 || time < best_t) { best = i; best_t = time; }
   }
   return best;
 }
 
+struct PlanEntry { int M, N, K; size_t part_elems; int tile, splits, split_row0; };
+std::mutex g_plan_mu;
+PlanEntry g_plans[32];
+int g_n_plans = 0;
+
 template <int BM, int BN, int WM, int WN, int EPI>
 hipError_t launch_one(const GemmCall& c, hipStream_t st) {
   if constexpr (tile_epi(BM, BN, WM, WN, EPI)) {
-    const int tiles = ((c.M + BM - 1) / BM) * (c.N / BN);
-    const int splits = EPI == EPI_PARTIAL && c.splits > 1 ? c.splits : 1;
-    gemm_kernel<BM, BN, WM, WN, EPI><<<dim3(tiles, splits), dim3(WM * WN * 64), 0, st>>>(c);
+    const int nTM = (c.M + BM - 1) / BM, nTN = c.N / BN;
+    int units = nTM * nTN;
+    if (EPI == EPI_RESIDUAL && c.splits > 1) {
+      const int mainTM = c.split_row0 / BM;
+      units = mainTM * nTN + (nTM - mainTM) * nTN * c.splits;
+    }
+    gemm_kernel<BM, BN, WM, WN, EPI><<<dim3(units), dim3(WM * WN * 64), 0, st>>>(c);
     return hipGetLastError();
   } else {
     return hipErrorInvalidValue;
@@ -597,7 +675,6 @@ hipError_t launch_cfg(const GemmCall& c, hipStream_t st) {
     case EPI_SWIGLU: return launch_one<BM, BN, WM, WN, EPI_SWIGLU>(c, st);
     case EPI_LMSTATS: return launch_one<BM, BN, WM, WN, EPI_LMSTATS>(c, st);
     case EPI_STORE_F32: return launch_one<BM, BN, WM, WN, EPI_STORE_F32>(c, st);
-    case EPI_PARTIAL: return launch_one<BM, BN, WM, WN, EPI_PARTIAL>(c, st);
     case EPI_LOGITS: return launch_one<BM, BN, WM, WN, EPI_LOGITS>(c, st);
   }
   return hipErrorInvalidValue;
@@ -605,26 +682,52 @@ hipError_t launch_cfg(const GemmCall& c, hipStream_t st) {
 
 }  // namespace
 
-int gemm_residual_splits(const GemmCall& c, int max_splits) {
-  const char* e = std::getenv("WINO_GEMM_SPLIT");
-  const int nk = c.K / BK;
-  if (e) {
-    const int s = std::atoi(e);
-    return (s >= 1 && s <= max_splits && nk % s == 0) ? s : 1;
-  }
-  double best_t = 0;
-  int best = 1;
-  for (int s = 1; s <= max_splits; ++s) {
-    if (nk % s || nk / s < 8) continue;  // keep >= 8 K steps per split
-    GemmCall p = c;
-    p.epi = s > 1 ? EPI_PARTIAL : c.epi;
-    for (int i = 0; i < kNumTiles; ++i) {
-      if (!tile_ok(p, kTiles[i])) continue;
-      const double t = tile_time(c, kTiles[i], s);
-      if (best_t == 0 || t < best_t) { best_t = t; best = s; }
+void plan_residual_gemm(GemmCall& c, size_t part_elems) {
+  const int f_tile = env_int("WINO_GEMM_TILE", -1);
+  const int f_split = env_int("WINO_GEMM_SPLIT", 0), f_tail = env_int("WINO_GEMM_TAIL", -1);
+  const bool forced = f_tile >= 0 || f_split > 0 || f_tail >= 0;
+  if (!forced) {
+    std::lock_guard<std::mutex> lk(g_plan_mu);
+    for (int i = 0; i < g_n_plans; ++i) {
+      const PlanEntry& e = g_plans[i];
+      if (e.M == c.M && e.N == c.N && e.K == c.K && e.part_elems == part_elems) {
+        c.tile = e.tile; c.splits = e.splits; c.split_row0 = e.split_row0;
+        return;
+      }
     }
   }
-  return best;
+  const int nk = c.K / BK;
+  int best = -1, best_s = 1, best_tail = 0;
+  double best_t = 0;
+  c.epi = EPI_RESIDUAL;
+  for (int i = 0; i < kNumTiles; ++i) {
+    const TileCfg& t = kTiles[i];
+    if (!tile_ok(c, t) || (f_tile >= 0 && i != f_tile)) continue;
+    const int nTM = (c.M + t.BM - 1) / t.BM;
+    for (int tail = 0; tail <= nTM; ++tail) {
+      if (f_tail >= 0 && tail != std::min(f_tail, nTM)) continue;
+      const double tail_rows = c.M - (double)(nTM - tail) * t.BM;
+      for (int s = tail ? 2 : 1; s <= (tail ? kMaxResidualSplits : 1); ++s) {
+        if (tail && (nk % s || nk / s < 4 || s * tail_rows * c.N > (double)part_elems)) continue;
+        if (tail && f_split > 0 && s != f_split) continue;
+        const double time = residual_time(c, t, tail, s);
+        if (best < 0 || time < best_t) { best = i; best_t = time; best_s = s; best_tail = tail; }
+      }
+    }
+  }
+  if (best < 0) {  // no candidate under the overrides: plain whole-K tiles
+    c.tile = 0; c.splits = 1; c.split_row0 = c.M;
+    return;
+  }
+  const int nTM = (c.M + kTiles[best].BM - 1) / kTiles[best].BM;
+  c.tile = best + 1;
+  c.splits = best_tail ? best_s : 1;
+  c.split_row0 = best_tail ? (nTM - best_tail) * kTiles[best].BM : c.M;
+  if (!forced) {
+    std::lock_guard<std::mutex> lk(g_plan_mu);
+    g_plans[g_n_plans % 32] = PlanEntry{c.M, c.N, c.K, part_elems, c.tile, c.splits, c.split_row0};
+    g_n_plans = std::min(g_n_plans + 1, 32);
+  }
 }
 
 int gemm_tile_n(const GemmCall& c) {
@@ -633,9 +736,15 @@ int gemm_tile_n(const GemmCall& c) {
 }
 
 hipError_t launch_gemm(const GemmCall& c, hipStream_t st) {
-  const int i = pick_tile(c);
-  if (i < 0) return hipErrorInvalidValue;
+  const int i = (c.tile > 0 && c.tile <= kNumTiles) ? c.tile - 1 : pick_tile(c);
+  if (i < 0 || !tile_ok(c, kTiles[i])) return hipErrorInvalidValue;
   if (c.M <= 0) return hipSuccess;
+  if (c.epi == EPI_RESIDUAL && c.splits > 1) {
+    const int nk = c.K / BK;
+    if (!c.part || c.split_row0 < 0 || c.split_row0 >= c.M || c.split_row0 % kTiles[i].BM ||
+        nk % c.splits)
+      return hipErrorInvalidValue;
+  }
   switch (i) {
     case 0: return launch_cfg<256, 256, 2, 2>(c, st);
     case 1: return launch_cfg<192, 256, 2, 2>(c, st);

@@ -104,31 +104,49 @@ __device__ __forceinline__ float load_row_f32(const float* xr, int d, int lane, 
 }
 
 // x[m] (+)= sum of split-K partials, in split order; returns the row in v.
+// The loads of one split for all of the lane's chunks are independent, so
+// they are in flight together.
 template <int CPL>
 __device__ __forceinline__ float load_row_reduce(float* xr, const float* part, int n_part,
                                                  size_t pstride, int d, int lane, float (&v)[CPL][8]) {
   const int nch = d >> 3;
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) {
+    const int ch = lane + c * 64;
+    if (ch < nch) {
+      const float4* xi = reinterpret_cast<const float4*>(xr + ch * 8);
+      const float4 a = xi[0], b = xi[1];
+      v[c][0] = a.x; v[c][1] = a.y; v[c][2] = a.z; v[c][3] = a.w;
+      v[c][4] = b.x; v[c][5] = b.y; v[c][6] = b.z; v[c][7] = b.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[c][e] = 0.f;
+    }
+  }
+  for (int s = 0; s < n_part; ++s) {
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const int ch = lane + c * 64;
+      if (ch < nch) {
+        const float4* pi = reinterpret_cast<const float4*>(part + s * pstride + ch * 8);
+        const float4 a = pi[0], b = pi[1];
+        v[c][0] += a.x; v[c][1] += a.y; v[c][2] += a.z; v[c][3] += a.w;
+        v[c][4] += b.x; v[c][5] += b.y; v[c][6] += b.z; v[c][7] += b.w;
+      }
+    }
+  }
   float ss = 0.f;
 #pragma unroll
   for (int c = 0; c < CPL; ++c) {
     const int ch = lane + c * 64;
     if (ch < nch) {
-      float4* xi = reinterpret_cast<float4*>(xr + ch * 8);
-      float4 a = xi[0], bq = xi[1];
-      for (int s = 0; s < n_part; ++s) {
-        const float4* pi = reinterpret_cast<const float4*>(part + s * pstride + ch * 8);
-        const float4 pa = pi[0], pb = pi[1];
-        a.x += pa.x; a.y += pa.y; a.z += pa.z; a.w += pa.w;
-        bq.x += pb.x; bq.y += pb.y; bq.z += pb.z; bq.w += pb.w;
+      if (n_part) {
+        float4* xo = reinterpret_cast<float4*>(xr + ch * 8);
+        xo[0] = make_float4(v[c][0], v[c][1], v[c][2], v[c][3]);
+        xo[1] = make_float4(v[c][4], v[c][5], v[c][6], v[c][7]);
       }
-      if (n_part) { xi[0] = a; xi[1] = bq; }
-      v[c][0] = a.x; v[c][1] = a.y; v[c][2] = a.z; v[c][3] = a.w;
-      v[c][4] = bq.x; v[c][5] = bq.y; v[c][6] = bq.z; v[c][7] = bq.w;
 #pragma unroll
       for (int e = 0; e < 8; ++e) ss += v[c][e] * v[c][e];
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[c][e] = 0.f;
     }
   }
   return ss;
@@ -138,25 +156,32 @@ template <int CPL>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x,
                                                       const uint16_t* __restrict__ gain, float eps,
                                                       int M, int d, uint16_t* __restrict__ h,
-                                                      const float* __restrict__ part, int n_part) {
+                                                      const float* __restrict__ part, int n_part,
+                                                      int part_row0) {
   const int lane = threadIdx.x & 63;
-  const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (m >= M) return;
+  // rows carrying partials (m >= part_row0) are the slow ones: take them first
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= M) return;
+  const int n_tail = n_part ? M - part_row0 : 0;
+  const int m = r < n_tail ? part_row0 + r : r - n_tail;
   float v[CPL][8];
-  const float ss = load_row_reduce<CPL>(x + (size_t)m * d, part + (size_t)m * d, n_part,
-                                        (size_t)M * d, d, lane, v);
+  const bool has = m >= part_row0;
+  const float ss = load_row_reduce<CPL>(x + (size_t)m * d, part + (size_t)(has ? m - part_row0 : 0) * d,
+                                        has ? n_part : 0, (size_t)(M - part_row0) * d, d, lane, v);
   norm_store<CPL>(v, ss, gain, eps, d, lane, h + (size_t)m * d);
 }
 
 template <int CPL>
 __global__ __launch_bounds__(256) void residual_reduce_kernel(float* __restrict__ x,
                                                               const float* __restrict__ part,
-                                                              int n_part, int M, int d) {
+                                                              int n_part, int part_row0, int M,
+                                                              int d) {
   const int lane = threadIdx.x & 63;
-  const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int m = part_row0 + blockIdx.x * 4 + (threadIdx.x >> 6);
   if (m >= M) return;
   float v[CPL][8];
-  load_row_reduce<CPL>(x + (size_t)m * d, part + (size_t)m * d, n_part, (size_t)M * d, d, lane, v);
+  load_row_reduce<CPL>(x + (size_t)m * d, part + (size_t)(m - part_row0) * d, n_part,
+                       (size_t)(M - part_row0) * d, d, lane, v);
 }
 
 template <int CPL>
@@ -203,20 +228,23 @@ void launch_embed_norm(const StepGeom& g, const int32_t* tokens, const uint16_t*
 }
 
 void launch_rmsnorm(float* x, const uint16_t* gain, float eps, int M, int d, uint16_t* h,
-                    const float* part, int n_part, hipStream_t st) {
-  dim3 grid((M + 3) / 4), block(256);
-  if (d <= 512) rmsnorm_kernel<1><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part);
-  else if (d <= 1024) rmsnorm_kernel<2><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part);
-  else if (d <= 2048) rmsnorm_kernel<4><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part);
-  else rmsnorm_kernel<8><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part);
+                    const float* part, int n_part, int part_row0, hipStream_t st) {
+  const dim3 grid((M + 3) / 4), block(256);
+  if (!part) n_part = 0;
+  if (d <= 512) rmsnorm_kernel<1><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
+  else if (d <= 1024) rmsnorm_kernel<2><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
+  else if (d <= 2048) rmsnorm_kernel<4><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
+  else rmsnorm_kernel<8><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
 }
 
-void launch_residual_reduce(float* x, const float* part, int n_part, int M, int d, hipStream_t st) {
-  dim3 grid((M + 3) / 4), block(256);
-  if (d <= 512) residual_reduce_kernel<1><<<grid, block, 0, st>>>(x, part, n_part, M, d);
-  else if (d <= 1024) residual_reduce_kernel<2><<<grid, block, 0, st>>>(x, part, n_part, M, d);
-  else if (d <= 2048) residual_reduce_kernel<4><<<grid, block, 0, st>>>(x, part, n_part, M, d);
-  else residual_reduce_kernel<8><<<grid, block, 0, st>>>(x, part, n_part, M, d);
+void launch_residual_reduce(float* x, const float* part, int n_part, int part_row0, int M, int d,
+                            hipStream_t st) {
+  if (M - part_row0 <= 0) return;
+  const dim3 grid((M - part_row0 + 3) / 4), block(256);
+  if (d <= 512) residual_reduce_kernel<1><<<grid, block, 0, st>>>(x, part, n_part, part_row0, M, d);
+  else if (d <= 1024) residual_reduce_kernel<2><<<grid, block, 0, st>>>(x, part, n_part, part_row0, M, d);
+  else if (d <= 2048) residual_reduce_kernel<4><<<grid, block, 0, st>>>(x, part, n_part, part_row0, M, d);
+  else residual_reduce_kernel<8><<<grid, block, 0, st>>>(x, part, n_part, part_row0, M, d);
 }
 
 void launch_select_norm(const StepGeom& g, int mode, const int32_t* tokens, const float* x,

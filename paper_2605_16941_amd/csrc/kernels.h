@@ -34,12 +34,15 @@ void launch_embed_norm(const StepGeom& g, const int32_t* tokens, const uint16_t*
                        const uint16_t* gain, float eps, int d, float* x, uint16_t* h,
                        hipStream_t st);
 // h[m] = rmsnorm(x[m]) * gain for m < M.  With n_part > 0 the split-K
-// partials part[s][m] (s < n_part, fp32 [n_part, M, d]) are first added to
-// x[m] in order s = 0, 1, ... and x is written back.
+// partials of rows m >= part_row0, part[s][m - part_row0] (s < n_part, fp32
+// [n_part, M - part_row0, d]), are first added to x[m] in order s = 0, 1, ...
+// and x is written back.
 void launch_rmsnorm(float* x, const uint16_t* gain, float eps, int M, int d, uint16_t* h,
-                    const float* part, int n_part, hipStream_t st);
-// x[m] += sum_s part[s][m] (same order as above), for m < M.
-void launch_residual_reduce(float* x, const float* part, int n_part, int M, int d, hipStream_t st);
+                    const float* part, int n_part, int part_row0, hipStream_t st);
+// x[m] += sum_s part[s][m - part_row0] (same order as above), for
+// part_row0 <= m < M.
+void launch_residual_reduce(float* x, const float* part, int n_part, int part_row0, int M, int d,
+                            hipStream_t st);
 // Rows the decision reads.  mode 0: one row per block position (current row
 // if the token is the mask, else the shadow row) and target = current token
 // (-1 for masked).  mode 1: all 2*Lb rows (current then shadow) per sequence.
@@ -74,14 +77,19 @@ struct LmStatsOut {   // LM head + streaming softmax statistics per (row, N-tile
 enum GemmEpi {
   EPI_QKV_ROPE = 0, EPI_RESIDUAL = 1, EPI_SWIGLU = 2, EPI_LMSTATS = 3,
   EPI_STORE_F32 = 4,  // out = A W^T (plain bf16 A)
-  EPI_LOGITS = 5,     // out = (A + A2) W^T + bias (LM-head precision, test entry point)
-  EPI_PARTIAL = 6     // split-K: out[split][M][N] = A W^T over that split's K range
+  EPI_LOGITS = 5      // out = (A + A2) W^T + bias (LM-head precision, test entry point)
 };
+constexpr int kMaxResidualSplits = 8;
 
 struct GemmCall {
-  // splits > 1 (EPI_PARTIAL only): K is the per-split depth; split s reads
-  // columns [s*K, (s+1)*K) of A and W and writes out + s*M*ldc
-  int splits;
+  int tile;  // 1 + tile shape index; 0 (zero-initialised call): chosen per call
+  // Residual epilogue only: rows [0, split_row0) are computed over the whole
+  // K and added to outf; with splits > 1 each tile of rows [split_row0, M) is
+  // computed as `splits` K-slices (slice s covers columns [s*K/splits,
+  // (s+1)*K/splits)) that write fp32 partials part[s][m - split_row0][n]
+  // (row stride N) for the next norm kernel to add.
+  int splits, split_row0;
+  float* part;
   const uint16_t* A; int lda;
   // LM-head epilogues take A as an unevaluated sum A + A2 of two bf16 parts
   // (hi and lo of an fp32 row): both are multiplied with the same W tile.
@@ -102,11 +110,13 @@ struct GemmCall {
 // environment variable WINO_GEMM_TILE=<index> forces one tile shape (tuning).
 int gemm_tile_n(const GemmCall& c);
 hipError_t launch_gemm(const GemmCall& c, hipStream_t st);
-// K splits worth using for a residual-add GEMM of this shape (1 = none): a
-// split-K run writes fp32 partials that the next RMSNorm (or
-// launch_residual_reduce) adds into the residual stream.  max_rows bounds
-// the partial buffer.  WINO_GEMM_SPLIT=<n> forces n (tuning).
-int gemm_residual_splits(const GemmCall& c, int max_splits);
+// Plans a residual-add GEMM: tile shape and how many trailing row tiles are
+// split over K (and how many ways), from a throughput model of whole-K tiles
+// and thin K-slices filling the CUs; writes tile, splits and split_row0 into
+// c.  part_elems bounds splits * (M - split_row0) * N.  The environment
+// variables WINO_GEMM_TILE, WINO_GEMM_SPLIT and WINO_GEMM_TAIL (row tiles in
+// the split tail) force choices (tuning).
+void plan_residual_gemm(GemmCall& c, size_t part_elems);
 
 // --------------------------------------------------------------- attention
 // Bidirectional attention with the WINO shadow mask (Sec. 4.2.2): query row

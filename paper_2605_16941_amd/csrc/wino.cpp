@@ -180,21 +180,29 @@ StepGeom make_geom(const wino_params* p, const int32_t* block_start) {
   return g;
 }
 
-// Residual-add GEMM, split over K when that fills the chip better: the fp32
-// partials land in the workspace and the caller adds them to x (fused into
-// the next RMSNorm).  Returns the number of pending partials (0 = added).
-int residual_gemm(wino_ctx* c, GemmCall g, hipStream_t st, hipError_t* err) {
-  const int cap = (int)std::min<size_t>(kMaxSplits, c->L.part_elems / ((size_t)g.M * g.N));
-  const int splits = cap > 1 ? gemm_residual_splits(g, cap) : 1;
-  if (splits > 1) {
-    g.epi = EPI_PARTIAL;
-    g.splits = splits;
-    g.K /= splits;
-    g.outf = c->part();
-    g.ldc = g.N;
-  }
+// Split-K partials of a residual GEMM not yet added to x: n splits of the
+// rows from row0 on.
+struct Pending {
+  int n = 0, row0 = 0;
+};
+
+// Residual-add GEMM.  When the planner splits the trailing row tiles over K,
+// their fp32 partials land in the workspace and the caller adds them to x
+// (fused into the next RMSNorm).
+Pending residual_gemm(wino_ctx* c, GemmCall g, hipStream_t st, hipError_t* err) {
+  g.part = c->part();
+  plan_residual_gemm(g, c->L.part_elems);
   *err = launch_gemm(g, st);
-  return splits > 1 ? splits : 0;
+  Pending p;
+  if (g.splits > 1) { p.n = g.splits; p.row0 = g.split_row0; }
+  return p;
+}
+
+// Bytes an RMSNorm moves: x read (and written back when partials are added),
+// h written, partials read.
+double norm_bytes(int M, int d, const Pending& p) {
+  const double rows = p.n ? M - p.row0 : 0;
+  return (double)M * d * 6 + rows * d * 4 + 4.0 * rows * d * p.n;
 }
 
 // Embedding and the first n_sub sublayers (attention and FFN halves of each
@@ -204,7 +212,7 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
   const wino_model_config& m = c->cfg;
   const int d = m.d_model, F = m.d_ff, H = m.n_heads, hd = m.head_dim;
   const int M = g.B * g.T;
-  int pend = 0;  // split-K partials not yet added to x
+  Pending pend;  // split-K partials not yet added to x
   {
     Bracket br(c, K_EMBED_NORM, st);
     launch_embed_norm(g, tokens, c->tok_emb, m.vocab, c->attn_norm[0], m.rms_eps, d, c->x(), c->h(), st);
@@ -241,10 +249,10 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
     if (2 * l + 1 >= n_sub) break;
     {
       Bracket br(c, K_RMSNORM, st);
-      launch_rmsnorm(c->x(), c->ffn_norm[l], m.rms_eps, M, d, c->h(), pend ? c->part() : nullptr, pend, st);
+      launch_rmsnorm(c->x(), c->ffn_norm[l], m.rms_eps, M, d, c->h(), c->part(), pend.n, pend.row0, st);
       HIP_TRY(c, hipGetLastError());
-      br.done(0, (double)M * d * (6 + 8 * (pend ? 1 : 0)) + 4.0 * M * d * pend);
-      pend = 0;
+      br.done(0, norm_bytes(M, d, pend));
+      pend = Pending{};
     }
     GemmCall gc{};
     gc.A = c->h(); gc.lda = d; gc.W = c->w_gu[l]; gc.ldw = d;
@@ -266,18 +274,19 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
     }
     if (l + 1 < m.n_layers && 2 * (l + 1) < n_sub) {
       Bracket br(c, K_RMSNORM, st);
-      launch_rmsnorm(c->x(), c->attn_norm[l + 1], m.rms_eps, M, d, c->h(), pend ? c->part() : nullptr,
-                     pend, st);
+      launch_rmsnorm(c->x(), c->attn_norm[l + 1], m.rms_eps, M, d, c->h(), c->part(), pend.n,
+                     pend.row0, st);
       HIP_TRY(c, hipGetLastError());
-      br.done(0, (double)M * d * (6 + 8 * (pend ? 1 : 0)) + 4.0 * M * d * pend);
-      pend = 0;
+      br.done(0, norm_bytes(M, d, pend));
+      pend = Pending{};
     }
   }
-  if (pend) {
+  if (pend.n) {
     Bracket br(c, K_RMSNORM, st);
-    launch_residual_reduce(c->x(), c->part(), pend, M, d, st);
+    launch_residual_reduce(c->x(), c->part(), pend.n, pend.row0, M, d, st);
     HIP_TRY(c, hipGetLastError());
-    br.done(0, (double)M * d * 8 + 4.0 * M * d * pend);
+    const double rows = M - pend.row0;
+    br.done(0, rows * d * 8 + 4.0 * rows * d * pend.n);
   }
   return WINO_OK;
 }
