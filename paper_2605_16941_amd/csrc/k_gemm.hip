@@ -315,22 +315,42 @@ __device__ __forceinline__ void epi_lmstats(const GemmCall& c, f32x16 (&acc)[FM]
   }
 }
 
-template <int BM, int BN, int WM, int WN, int EPI>
-__global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
+// Physical 16-byte position of chunk kc of LDS tile row r: rows of KB bf16
+// (KB/8 chunks) are XOR-swizzled so the fragment reads of 8 or 16
+// consecutive rows at one chunk hit distinct bank groups.
+//   KB = 64 (128-byte rows): kc ^ ((r ^ (r >> 3)) & 7): any 8 consecutive rows
+//     use 8 positions, any 16 rows 16 (row parity, position) pairs.
+//   KB = 32 (64-byte rows, 4 per 64 banks): kc ^ ((r >> 2) & 3): 16
+//     consecutive rows give 16 distinct (r mod 4, position) pairs.
+template <int KB>
+__device__ __forceinline__ int lds_swz(int r) {
+  if constexpr (KB == 64) return (r ^ (r >> 3)) & 7;
+  else return (r >> 2) & 3;
+}
+
+// OCC workgroups per CU: the launch bound asks for OCC * waves / 4 waves per
+// SIMD, which caps the registers per wave accordingly.
+template <int BM, int BN, int WM, int WN, int EPI, int KB, int NST, int OCC>
+__global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_kernel(const GemmCall c) {
+  static_assert(KB == 32 || KB == 64, "K step");
+  static_assert(NST >= 2, "pipeline stages");
   constexpr int NW = WM * WN;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int FM = WTM / 32, FN = WTN / 32;
   // LM-head epilogues multiply W with both bf16 parts (hi, lo) of the fp32 rows
   constexpr bool SPLIT = EPI == EPI_LMSTATS || EPI == EPI_LOGITS;
   constexpr int AROWS = SPLIT ? 2 * BM : BM;
-  // one LDS-DMA instruction moves 64 lanes x 16 bytes = 8 tile rows of 64 bf16
-  constexpr int A_INS = AROWS / (8 * NW);
-  constexpr int B_INS = BN / (8 * NW);
-  static_assert(A_INS * 8 * NW == AROWS && B_INS * 8 * NW == BN, "loader split");
+  // one LDS-DMA instruction moves 64 lanes x 16 bytes = 1 KB = RPI tile rows
+  constexpr int CPR = KB / 8;    // 16-byte chunks per tile row
+  constexpr int RPI = 64 / CPR;  // tile rows per DMA instruction
+  constexpr int A_INS = AROWS / (RPI * NW);
+  constexpr int B_INS = BN / (RPI * NW);
+  constexpr int INS = A_INS + B_INS;
+  static_assert(A_INS * RPI * NW == AROWS && B_INS * RPI * NW == BN, "loader split");
   static_assert(FM >= 1 && FN >= 1, "wave tile");
-  constexpr int STAGE = (AROWS + BN) * BK;  // bf16 elements per pipeline stage
+  constexpr int STAGE = (AROWS + BN) * KB;  // bf16 elements per pipeline stage
 
-  __shared__ __attribute__((aligned(1024))) uint16_t smem[2 * STAGE];
+  __shared__ __attribute__((aligned(1024))) uint16_t smem[NST * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave - (wave / WN) * WN;
@@ -359,21 +379,16 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
   const int Ku = tail ? c.K / c.splits : c.K;  // K depth of this unit
   const int m0 = tm * BM, n0 = tn * BN;
 
-  // Tile rows are 128 bytes = 8 chunks of 16 bytes; chunk kc of row r is
-  // stored at position kc ^ swz(r), swz(r) = (r ^ (r >> 3)) & 7.  Any 8
-  // consecutive rows then use 8 different positions, and any 16 consecutive
-  // rows 16 different (row parity, position) pairs: the fragment reads of a
-  // wave hit distinct LDS banks whether 8 or 16 lanes are served per cycle.
-  // The lane that fills position (lane & 7) of row 8*i + lane/8 of a tile
-  // therefore fetches chunk (lane & 7) ^ ((lane/8 ^ i) & 7).
-  const int lrow = lane >> 3;
+  // The lane that fills position (lane % CPR) of row RPI*i + lane/CPR of a
+  // tile fetches the chunk that belongs there: position ^ lds_swz(row).
+  const int lrow = lane / CPR, lpos = lane % CPR;
   const int kbase = split * Ku;  // first K column of this unit
   const uint16_t* asrc[A_INS];
 #pragma unroll
   for (int i = 0; i < A_INS; ++i) {
     const int gi = wave * A_INS + i;
-    const int row = gi * 8 + lrow;
-    const int lkc = (lane & 7) ^ ((lrow ^ gi) & 7);
+    const int row = gi * RPI + lrow;
+    const int lkc = lpos ^ lds_swz<KB>(row);
     const bool lo = SPLIT && row >= BM;
     const int gm = min(m0 + (lo ? row - BM : row), c.M - 1);
     asrc[i] = (lo ? c.A2 : c.A) + (size_t)gm * c.lda + kbase + lkc * 8;
@@ -382,23 +397,23 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
 #pragma unroll
   for (int i = 0; i < B_INS; ++i) {
     const int gi = wave * B_INS + i;
-    const int lkc = (lane & 7) ^ ((lrow ^ gi) & 7);
-    const int vc = n0 + gi * 8 + lrow;
+    const int lkc = lpos ^ lds_swz<KB>(gi * RPI + lrow);
+    const int vc = n0 + gi * RPI + lrow;
     const int wr = EPI == EPI_SWIGLU ? swiglu_row<WTN>(vc, c.F) : vc;
     bsrc[i] = c.W + (size_t)wr * c.ldw + kbase + lkc * 8;
   }
 
   auto issue = [&](int kt, int stage) {
     uint16_t* sA = smem + stage * STAGE;
-    uint16_t* sB = sA + AROWS * BK;
+    uint16_t* sB = sA + AROWS * KB;
 #pragma unroll
     for (int i = 0; i < A_INS; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + kt * BK),
+      __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + kt * KB),
                                        (__attribute__((address_space(3))) void*)(sA + (wave * A_INS + i) * 512),
                                        16, 0, 0);
 #pragma unroll
     for (int i = 0; i < B_INS; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(bsrc[i] + kt * BK),
+      __builtin_amdgcn_global_load_lds((const void*)(bsrc[i] + kt * KB),
                                        (__attribute__((address_space(3))) void*)(sB + (wave * B_INS + i) * 512),
                                        16, 0, 0);
   };
@@ -411,22 +426,22 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[fm][fn][i] = 0.f;
 
-  const int nk = Ku / BK;
+  const int nk = Ku / KB;
   const int arow = wm * WTM + (lane & 31), brow = wn * WTN + (lane & 31);
   // swizzle of each fragment row this lane reads (fixed over the K loop)
   int aswz[FM], alswz[SPLIT ? FM : 1], bswz[FN];
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) {
     const int r = arow + fm * 32;
-    aswz[fm] = (r ^ (r >> 3)) & 7;
-    if constexpr (SPLIT) alswz[fm] = ((BM + r) ^ ((BM + r) >> 3)) & 7;
+    aswz[fm] = lds_swz<KB>(r);
+    if constexpr (SPLIT) alswz[fm] = lds_swz<KB>(BM + r);
   }
 #pragma unroll
   for (int fn = 0; fn < FN; ++fn) {
     const int r = brow + fn * 32;
-    bswz[fn] = (r ^ (r >> 3)) & 7;
+    bswz[fn] = lds_swz<KB>(r);
   }
-  constexpr int KS = BK / 16;
+  constexpr int KS = KB / 16;
   constexpr int NR = FM + FN + (SPLIT ? FM : 0);   // LDS fragment reads per 16-deep step
   constexpr int NM = FM * FN * (SPLIT ? 2 : 1);     // MFMAs per step
   constexpr int RI = NR < NM ? NR : NM;              // reads interleaved with MFMAs
@@ -434,21 +449,21 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
 
   bf16x8 af[2][FM], bf[2][FN], al[2][SPLIT ? FM : 1];
   auto load_frags = [&](const uint16_t* sA, int ks, int buf) {
-    const uint16_t* sB = sA + AROWS * BK;
+    const uint16_t* sB = sA + AROWS * KB;
     const int kc = ks * 2 + (lane >> 5);
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
       af[buf][fm] = as_bf16x8(*reinterpret_cast<const uint4*>(
-          sA + (arow + fm * 32) * BK + ((kc ^ aswz[fm]) << 3)));
+          sA + (arow + fm * 32) * KB + ((kc ^ aswz[fm]) << 3)));
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn)
       bf[buf][fn] = as_bf16x8(*reinterpret_cast<const uint4*>(
-          sB + (brow + fn * 32) * BK + ((kc ^ bswz[fn]) << 3)));
+          sB + (brow + fn * 32) * KB + ((kc ^ bswz[fn]) << 3)));
     if constexpr (SPLIT) {
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
         al[buf][fm] = as_bf16x8(*reinterpret_cast<const uint4*>(
-            sA + (BM + arow + fm * 32) * BK + ((kc ^ alswz[fm]) << 3)));
+            sA + (BM + arow + fm * 32) * KB + ((kc ^ alswz[fm]) << 3)));
     }
   };
   auto mfmas = [&](int buf) {
@@ -482,33 +497,32 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
     }
   };
 
-  // Pipeline: tile t sits in LDS stage t&1; its DMA is issued two tiles
-  // ahead.  Crossing from tile t to t+1, each wave (1) waits for its copies
-  // of tile t+1, (2) meets the others at the barrier - after which every
-  // wave has read all of tile t, (3) issues tile t+2 into tile t's stage,
-  // (4) issues the first fragment reads of tile t+1, and only then (5) runs
-  // the last MFMAs of tile t, which cover the latency of those reads.
-  issue(0, 0);
-  if (nk > 1) {
-    issue(1, 1);
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(A_INS + B_INS) : "memory");
-  } else {
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  }
+  // Pipeline over NST LDS stages: K tile t sits in stage t % NST and its DMA
+  // is issued NST tiles ahead.  Crossing from tile t to t+1, each wave (1)
+  // waits for its copies of tile t+1 (the NST-2 later tiles may still be in
+  // flight), (2) meets the others at the barrier - after which every wave
+  // has read all of tile t, (3) issues tile t+NST into tile t's stage, (4)
+  // issues the first fragment reads of tile t+1, and only then (5) runs the
+  // last MFMAs of tile t, which cover the latency of those reads.  Tiles past
+  // the end are refetches of the last one, which keeps the wait counts fixed.
+#pragma unroll
+  for (int s0 = 0; s0 < NST; ++s0) issue(s0 < nk ? s0 : nk - 1, s0);
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NST - 1) * INS) : "memory");
   __syncthreads();
   load_frags(smem, 0, 0);
+  int cur = 0;  // stage of tile kt
   for (int kt = 0; kt + 1 < nk; ++kt) {
-    const uint16_t* sA = smem + (kt & 1) * STAGE;
-    inner_steps(sA);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    inner_steps(smem + cur * STAGE);
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NST - 2) * INS) : "memory");
     __syncthreads();
-    issue(kt + 2 < nk ? kt + 2 : nk - 1, kt & 1);  // the last one only refetches
-    load_frags(smem + ((kt + 1) & 1) * STAGE, 0, 0);
+    issue(kt + NST < nk ? kt + NST : nk - 1, cur);
+    cur = cur + 1 == NST ? 0 : cur + 1;
+    load_frags(smem + cur * STAGE, 0, 0);
     mfmas((KS - 1) & 1);
     __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
   }
-  inner_steps(smem + ((nk - 1) & 1) * STAGE);
+  inner_steps(smem + cur * STAGE);
   mfmas((KS - 1) & 1);
   // the refetch issued last may still be landing: finish it before the
   // epilogue reuses LDS
@@ -524,7 +538,7 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
   else if constexpr (EPI == EPI_SWIGLU) epi_swiglu<FM, FN>(c, acc, rowb, colb, lane);
   else if constexpr (EPI == EPI_QKV_ROPE) {
     // each wave stages its WTM x WTN tile in its own LDS region
-    static_assert(BM * BN <= 2 * STAGE, "QKV staging fits the pipeline LDS");
+    static_assert(BM * BN <= NST * STAGE, "QKV staging fits the pipeline LDS");
     epi_qkv_rope<FM, FN>(c, acc, rowb, colb, lane, smem + wave * (WTM * WTN));
   }
   else epi_lmstats<BM, WM, WN, FM, FN>(c, acc, m0, tn, rowb, colb, lane, wm, wn, smem);
@@ -532,21 +546,26 @@ __global__ __launch_bounds__(WM* WN * 64) void gemm_kernel(const GemmCall c) {
 
 struct TileCfg {
   int BM, BN, WM, WN;
-  int occ;     // workgroups a CU holds at once (LDS / registers)
-  float eff;   // relative per-CU matrix-core throughput when the chip is full
-               // (measured on the 8704x24576x4096 gate/up shape)
+  int KB, NST;  // K step of a pipeline stage, number of LDS stages
+  int occ;      // workgroups a CU holds at once (LDS / registers)
+  float eff;    // relative per-CU matrix-core throughput when the chip is full
+                // (measured on the 8704x24576x4096 gate/up shape)
 };
 
+// eff: measured relative throughput of each shape (8704 x 24576 x 4096, and
+// the O / down residual shapes for the 192-row tile, whose single wave per
+// SIMD exposes the residual read-add-write).  Deeper pipelines of 32-deep K
+// stages and two-per-CU 128x256 tiles were measured slower than entry 6.
 constexpr TileCfg kTiles[] = {
-    {256, 256, 2, 2, 1, 0.94f},  // 0
-    {192, 256, 2, 2, 1, 0.90f},  // 1
-    {128, 256, 2, 2, 1, 0.75f},  // 2
-    {128, 128, 2, 2, 2, 0.77f},  // 3
-    {64, 128, 2, 2, 3, 0.65f},   // 4
-    {32, 256, 1, 4, 2, 0.95f},   // 5
-    {256, 256, 4, 2, 1, 1.00f},  // 6  (8 waves)
-    {256, 256, 2, 4, 1, 0.99f},  // 7  (8 waves)
-    {128, 256, 2, 4, 1, 0.76f},  // 8  (8 waves)
+    {256, 256, 2, 2, 64, 2, 1, 0.95f},  // 0
+    {192, 256, 2, 2, 64, 2, 1, 0.75f},  // 1
+    {128, 256, 2, 2, 64, 2, 1, 0.76f},  // 2
+    {128, 128, 2, 2, 64, 2, 2, 0.78f},  // 3
+    {64, 128, 2, 2, 64, 2, 3, 0.64f},   // 4
+    {32, 256, 1, 4, 64, 2, 2, 0.95f},   // 5
+    {256, 256, 4, 2, 64, 2, 1, 1.00f},  // 6  (8 waves)
+    {256, 256, 2, 4, 64, 2, 1, 0.98f},  // 7  (8 waves)
+    {128, 256, 2, 4, 64, 2, 1, 0.74f},  // 8  (8 waves)
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 
@@ -564,6 +583,9 @@ constexpr bool tile_epi(int BM, int BN, int WM, int WN, int EPI) {
 bool tile_ok(const GemmCall& c, const TileCfg& t) {
   if (c.N % t.BN || c.K % BK) return false;
   if (!tile_epi(t.BM, t.BN, t.WM, t.WN, c.epi)) return false;
+  const int arows = (c.epi == EPI_LMSTATS || c.epi == EPI_LOGITS) ? 2 * t.BM : t.BM;
+  if (t.occ * t.NST * (arows + t.BN) * t.KB * 2 > 160 * 1024) return false;
+  if (c.epi == EPI_QKV_ROPE && t.BM * t.BN > t.NST * (t.BM + t.BN) * t.KB) return false;
   const int WTN = t.BN / t.WN;
   if (c.epi == EPI_QKV_ROPE) return WTN == c.rope.hd && (c.rope.H * c.rope.hd) % t.BN == 0;
   if (c.epi == EPI_SWIGLU) return (c.F % (WTN / 2)) == 0;
@@ -651,31 +673,34 @@ std::mutex g_plan_mu;
 PlanEntry g_plans[32];
 int g_n_plans = 0;
 
-template <int BM, int BN, int WM, int WN, int EPI>
+template <int BM, int BN, int WM, int WN, int EPI, int KB, int NST, int OCC>
 hipError_t launch_one(const GemmCall& c, hipStream_t st) {
-  if constexpr (tile_epi(BM, BN, WM, WN, EPI)) {
+  constexpr int arows = (EPI == EPI_LMSTATS || EPI == EPI_LOGITS) ? 2 * BM : BM;
+  constexpr int lds = NST * (arows + BN) * KB * 2;
+  constexpr bool qkv_fits = EPI != EPI_QKV_ROPE || BM * BN <= NST * (BM + BN) * KB;
+  if constexpr (tile_epi(BM, BN, WM, WN, EPI) && lds * OCC <= 160 * 1024 && qkv_fits) {
     const int nTM = (c.M + BM - 1) / BM, nTN = c.N / BN;
     int units = nTM * nTN;
     if (EPI == EPI_RESIDUAL && c.splits > 1) {
       const int mainTM = c.split_row0 / BM;
       units = mainTM * nTN + (nTM - mainTM) * nTN * c.splits;
     }
-    gemm_kernel<BM, BN, WM, WN, EPI><<<dim3(units), dim3(WM * WN * 64), 0, st>>>(c);
+    gemm_kernel<BM, BN, WM, WN, EPI, KB, NST, OCC><<<dim3(units), dim3(WM * WN * 64), 0, st>>>(c);
     return hipGetLastError();
   } else {
     return hipErrorInvalidValue;
   }
 }
 
-template <int BM, int BN, int WM, int WN>
+template <int BM, int BN, int WM, int WN, int KB, int NST, int OCC>
 hipError_t launch_cfg(const GemmCall& c, hipStream_t st) {
   switch (c.epi) {
-    case EPI_QKV_ROPE: return launch_one<BM, BN, WM, WN, EPI_QKV_ROPE>(c, st);
-    case EPI_RESIDUAL: return launch_one<BM, BN, WM, WN, EPI_RESIDUAL>(c, st);
-    case EPI_SWIGLU: return launch_one<BM, BN, WM, WN, EPI_SWIGLU>(c, st);
-    case EPI_LMSTATS: return launch_one<BM, BN, WM, WN, EPI_LMSTATS>(c, st);
-    case EPI_STORE_F32: return launch_one<BM, BN, WM, WN, EPI_STORE_F32>(c, st);
-    case EPI_LOGITS: return launch_one<BM, BN, WM, WN, EPI_LOGITS>(c, st);
+    case EPI_QKV_ROPE: return launch_one<BM, BN, WM, WN, EPI_QKV_ROPE, KB, NST, OCC>(c, st);
+    case EPI_RESIDUAL: return launch_one<BM, BN, WM, WN, EPI_RESIDUAL, KB, NST, OCC>(c, st);
+    case EPI_SWIGLU: return launch_one<BM, BN, WM, WN, EPI_SWIGLU, KB, NST, OCC>(c, st);
+    case EPI_LMSTATS: return launch_one<BM, BN, WM, WN, EPI_LMSTATS, KB, NST, OCC>(c, st);
+    case EPI_STORE_F32: return launch_one<BM, BN, WM, WN, EPI_STORE_F32, KB, NST, OCC>(c, st);
+    case EPI_LOGITS: return launch_one<BM, BN, WM, WN, EPI_LOGITS, KB, NST, OCC>(c, st);
   }
   return hipErrorInvalidValue;
 }
@@ -746,15 +771,15 @@ hipError_t launch_gemm(const GemmCall& c, hipStream_t st) {
       return hipErrorInvalidValue;
   }
   switch (i) {
-    case 0: return launch_cfg<256, 256, 2, 2>(c, st);
-    case 1: return launch_cfg<192, 256, 2, 2>(c, st);
-    case 2: return launch_cfg<128, 256, 2, 2>(c, st);
-    case 3: return launch_cfg<128, 128, 2, 2>(c, st);
-    case 4: return launch_cfg<64, 128, 2, 2>(c, st);
-    case 5: return launch_cfg<32, 256, 1, 4>(c, st);
-    case 6: return launch_cfg<256, 256, 4, 2>(c, st);
-    case 7: return launch_cfg<256, 256, 2, 4>(c, st);
-    case 8: return launch_cfg<128, 256, 2, 4>(c, st);
+    case 0: return launch_cfg<256, 256, 2, 2, 64, 2, 1>(c, st);
+    case 1: return launch_cfg<192, 256, 2, 2, 64, 2, 1>(c, st);
+    case 2: return launch_cfg<128, 256, 2, 2, 64, 2, 1>(c, st);
+    case 3: return launch_cfg<128, 128, 2, 2, 64, 2, 2>(c, st);
+    case 4: return launch_cfg<64, 128, 2, 2, 64, 2, 3>(c, st);
+    case 5: return launch_cfg<32, 256, 1, 4, 64, 2, 2>(c, st);
+    case 6: return launch_cfg<256, 256, 4, 2, 64, 2, 1>(c, st);
+    case 7: return launch_cfg<256, 256, 2, 4, 64, 2, 1>(c, st);
+    case 8: return launch_cfg<128, 256, 2, 4, 64, 2, 1>(c, st);
   }
   return hipErrorInvalidValue;
 }
