@@ -103,7 +103,9 @@ typedef struct {
   float z_best;   /* max logit over ids != mask_id                            */
   float z_target; /* logit of the current token (verify rows), else -inf      */
   int32_t argmax; /* lowest id reaching z_best                                */
-  int32_t row_kind; /* 0 current row (draft), 1 shadow row (verify), -1 idle  */
+  int32_t row_kind; /* 0 current row (draft), 1 shadow row (verify), -1 idle,
+                       2 unmasked position not verified: the step ran without
+                       the shadow block (tau2 <= 0, see wino_step)            */
 } wino_row_stats;
 
 /* Decision flags written per block position (uint8). */
@@ -132,7 +134,11 @@ size_t wino_workspace_bytes(const wino_model_config* cfg, int32_t max_batch, int
  *   d_n_masked    int32 [batch] masks left in Y_cur after the step, or NULL
  *   d_stats       wino_row_stats [batch, block_len], or NULL
  * Sequences that are done or whose Y_cur holds no mask are left unchanged
- * (flags 0, n_masked 0).  Asynchronous on `stream`. */
+ * (flags 0, n_masked 0).  With tau2 <= 0 no position can be re-masked (Eq. 3
+ * compares a probability), so the step runs without the shadow block; the
+ * decode loops below also drop it for steps in which every active sequence's
+ * Y_cur is all masks (Sec. 4.2.2: the other rows never see the shadow block,
+ * so the result is the same).  Asynchronous on `stream`. */
 wino_status wino_step(wino_ctx* ctx, const wino_params* p, int32_t* d_tokens,
                       const int32_t* d_block_start, int32_t* d_block_steps, uint8_t* d_flags,
                       int32_t* d_n_masked, wino_row_stats* d_stats, void* stream);

@@ -92,6 +92,7 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
       }
     }
     if (tid == 0 && a.n_masked) a.n_masked[b] = 0;
+    if (tid == 0 && a.next_verify) a.next_verify[b] = 0;
     return;
   }
 
@@ -111,7 +112,8 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
       s_val[l] = __expf(z - p.m) / p.s;  // Eq. 2 confidence / Eq. 3 probability
       s_hat[l] = p.i;
       if (stats) {
-        RowStats r = {p.m, p.s, p.b, masked ? kNegBig : p.t, p.i, masked ? 0 : 1};
+        const bool ver = !masked && (a.verify || a.standalone);
+        RowStats r = {p.m, p.s, p.b, ver ? p.t : kNegBig, p.i, masked ? 0 : (ver ? 1 : 2)};
         stats[row] = r;
       }
     }
@@ -126,7 +128,7 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
     if (masked) {
       if (cap_now) f = WINO_CAPFILL_FLAG;
       else if (s_val[l] > a.tau1) { f = WINO_DRAFT_FLAG; s_any_draft = 1; }
-    } else if (!cap_now && s_val[l] < a.tau2) {
+    } else if ((a.verify || a.standalone) && !cap_now && s_val[l] < a.tau2) {
       f = WINO_REMASK_FLAG;
     }
     s_flag[l] = f;
@@ -152,15 +154,57 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
     if (a.bitmap) a.bitmap[(size_t)b * Lb + l] = t == a.mask_id;
   }
   __syncthreads();
+  const bool adv = !a.standalone && a.advance && s_nmask_after == 0;
+  if (!a.standalone && a.next_verify) {
+    // the next step's Y_cur: this block, or the next one after an advance
+    int nmask = s_nmask_after, nkeep = Lb - s_nmask_after;
+    if (adv) {
+      const int nbs = a.block_start[b] + Lb;
+      if (tid == 0) { s_nmask = 0; s_any_draft = 0; }
+      __syncthreads();
+      if (nbs < a.G) {
+        const int32_t* nxt = a.tokens + (size_t)b * a.S + a.P + (nbs > a.G - Lb ? a.G - Lb : nbs);
+        for (int l = tid; l < Lb; l += 256) {
+          if (nxt[l] == a.mask_id) atomicAdd(&s_nmask, 1);
+          else atomicAdd(&s_any_draft, 1);
+        }
+      }
+      __syncthreads();
+      nmask = s_nmask;
+      nkeep = nbs < a.G ? s_any_draft : 0;
+    }
+    if (tid == 0) a.next_verify[b] = nmask > 0 && nkeep > 0;
+  }
   if (tid == 0) {
     if (a.n_masked) a.n_masked[b] = s_nmask_after;
     if (a.seq_steps) a.seq_steps[b] += 1;
     if (!a.standalone && a.block_steps) a.block_steps[b] = steps_before + 1;
-    if (!a.standalone && a.advance && s_nmask_after == 0) {
+    if (adv) {
       a.block_start[b] += Lb;
       if (a.block_steps) a.block_steps[b] = 0;
     }
   }
+}
+
+// next_verify[b] for a state before any step: the sequence is active and its
+// Y_cur holds both a mask and a non-mask token.
+__global__ __launch_bounds__(64) void probe_verify_kernel(const StepGeom g,
+                                                          const int32_t* __restrict__ tokens,
+                                                          int32_t* __restrict__ next_verify) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  const int bs = g.block_start[b];
+  int nmask = 0, nkeep = 0;
+  if (bs < g.G) {
+    const int32_t* cur = tokens + (size_t)b * g.S + cur_start(g, b);
+    for (int l = lane; l < g.Lb; l += 64) {
+      const bool m = cur[l] == g.mask_id;
+      nmask += m;
+      nkeep += !m;
+    }
+  }
+  nmask = (int)wave_sum((float)nmask);
+  nkeep = (int)wave_sum((float)nkeep);
+  if (lane == 0) next_verify[b] = nmask > 0 && nkeep > 0;
 }
 
 __global__ __launch_bounds__(256) void epi_stats_kernel(const uint16_t* __restrict__ logits,
@@ -238,6 +282,12 @@ __global__ __launch_bounds__(256) void epi_stats_kernel(const uint16_t* __restri
 }
 
 }  // namespace
+
+hipError_t launch_probe_verify(const StepGeom& g, const int32_t* tokens, int32_t* next_verify,
+                               hipStream_t st) {
+  probe_verify_kernel<<<g.B, 64, 0, st>>>(g, tokens, next_verify);
+  return hipGetLastError();
+}
 
 hipError_t launch_decide(const DecideArgs& a, hipStream_t st) {
   const size_t shm = (size_t)a.Lb * 16;

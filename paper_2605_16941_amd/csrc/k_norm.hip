@@ -201,9 +201,11 @@ __global__ __launch_bounds__(256) void select_norm_kernel(StepGeom g, int mode,
   int src;
   if (mode == 0) {
     const int tok = tokens[(size_t)b * g.S + c0 + j];
-    const bool masked = tok == g.mask_id;
-    src = masked ? c0 + j : g.S + j;  // Eq. 4: draft reads Y_cur, verify reads Y_shad
-    if (lane == 0) target[r] = masked ? -1 : tok;
+    // Eq. 4: draft reads Y_cur, verify reads Y_shad (without shadow rows no
+    // position is verified; the current row's statistics then go unused)
+    const bool verify = tok != g.mask_id && g.Ls > 0;
+    src = verify ? g.S + j : c0 + j;
+    if (lane == 0) target[r] = verify ? tok : -1;
   } else {
     src = j < g.Lb ? c0 + j : g.S + (j - g.Lb);
     if (lane == 0) target[r] = -1;

@@ -10,7 +10,11 @@ namespace wino {
 // residual stream holds B*T rows, row b*T + t.
 struct StepGeom {
   int B, P, G, Lb;      // batch, prompt length, generation length, block length
-  int S, T, Tp;         // S = P + G, T = S + Lb, Tp = T rounded up to 64
+  // Ls shadow rows follow the S = P + G sequence rows: Lb, or 0 for a step in
+  // which no position can be verified (Eq. 4 then reads current rows only, and
+  // the other rows never see the shadow block, so dropping it changes nothing).
+  int Ls;
+  int S, T, Tp;         // T = S + Ls, Tp = T rounded up to 64
   int mask_id;
   const int32_t* block_start;  // [B] generation-relative start of Y_cur
 };
@@ -148,8 +152,15 @@ struct DecideArgs {
   uint8_t* bitmap;       // [B, Lb] or null (standalone)
   int32_t* n_masked;     // [B] or null
   void* stats;           // wino_row_stats [B, Lb] or null
+  int verify;            // shadow rows were computed: the Eq. 3 rule applies
+  // [B] or null: 1 if the sequence's next step may verify (it is active and
+  // its next Y_cur holds both a mask and a drafted token), else 0
+  int32_t* next_verify;
 };
 hipError_t launch_decide(const DecideArgs& a, hipStream_t st);
+// next_verify[b] as above for the state before any step (fused-step layout).
+hipError_t launch_probe_verify(const StepGeom& g, const int32_t* tokens, int32_t* next_verify,
+                               hipStream_t st);
 
 // Standalone epilogue statistics: for each (b, l) pick the current row
 // (masked) or the shadow row (unmasked) of bf16 logits [B, 2Lb, V], and write

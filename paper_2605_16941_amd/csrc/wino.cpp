@@ -111,6 +111,7 @@ struct wino_ctx {
   int32_t* block_steps() const { return at<int32_t>(L.misc); }
   int32_t* seq_steps() const { return at<int32_t>(L.misc) + max_batch; }
   int32_t* n_masked() const { return at<int32_t>(L.misc) + 2 * max_batch; }
+  int32_t* next_verify() const { return at<int32_t>(L.misc) + 3 * max_batch; }
 
   hipEvent_t get_event() {
     if (!pool.empty()) { hipEvent_t e = pool.back(); pool.pop_back(); return e; }
@@ -171,10 +172,11 @@ wino_status validate_params(wino_ctx* ctx, const wino_params* p) {
   return WINO_OK;
 }
 
-StepGeom make_geom(const wino_params* p, const int32_t* block_start) {
+StepGeom make_geom(const wino_params* p, const int32_t* block_start, bool shadow = true) {
   StepGeom g{};
   g.B = p->batch; g.P = p->prompt_len; g.G = p->gen_len; g.Lb = p->block_len;
-  g.S = g.P + g.G; g.T = g.S + g.Lb; g.Tp = round64(g.T);
+  g.Ls = shadow ? g.Lb : 0;
+  g.S = g.P + g.G; g.T = g.S + g.Ls; g.Tp = round64(g.T);
   g.mask_id = p->mask_id;
   g.block_start = block_start;
   return g;
@@ -233,7 +235,7 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
     {
       Bracket br(c, K_ATTENTION, st);
       HIP_TRY(c, launch_attention(g, c->q(), c->k(), c->vt(), H, hd, c->att(), st));
-      const double pairs = (double)g.S * g.S + (double)g.Lb * (g.T - 1);
+      const double pairs = (double)g.S * g.S + (double)g.Ls * (g.T - 1);
       br.done(4.0 * hd * H * g.B * pairs, 2.0 * 4.0 * M * d);
     }
     GemmCall oc{};
@@ -291,11 +293,15 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
   return WINO_OK;
 }
 
+// One fused WINO step.  shadow = false drops the shadow block for a step in
+// which no position can be verified (tau2 <= 0, or every active sequence's
+// Y_cur is all masks): the other rows never see it and Eq. 4 reads only
+// current rows then, so the result is unchanged.
 wino_status step_impl(wino_ctx* c, const wino_params* p, int32_t* tokens, int32_t* block_start,
                       int32_t* block_steps, uint8_t* flags, int32_t* n_masked, void* stats,
-                      int advance, int32_t* seq_steps, hipStream_t st) {
+                      int advance, int32_t* seq_steps, bool shadow, hipStream_t st) {
   const wino_model_config& m = c->cfg;
-  const StepGeom g = make_geom(p, block_start);
+  const StepGeom g = make_geom(p, block_start, shadow);
   wino_status s = run_forward(c, g, tokens, 2 * m.n_layers, st);
   if (s != WINO_OK) return s;
   const int R = g.B * g.Lb;
@@ -334,6 +340,8 @@ wino_status step_impl(wino_ctx* c, const wino_params* p, int32_t* tokens, int32_
   da.block_start = block_start; da.block_steps = block_steps; da.advance = advance;
   da.seq_steps = seq_steps; da.flags = flags; da.bitmap = nullptr; da.n_masked = n_masked;
   da.stats = stats;
+  da.verify = shadow;
+  da.next_verify = c->next_verify();
   {
     Bracket br(c, K_DECIDE, st);
     HIP_TRY(c, launch_decide(da, st));
@@ -446,9 +454,24 @@ wino_status wino_step(wino_ctx* c, const wino_params* p, int32_t* d_tokens,
   wino_status s = validate_params(c, p);
   if (s != WINO_OK) return s;
   if (!d_tokens || !d_block_start) return WINO_ERR_INVALID_ARG;
+  // Eq. 3 can only fire with tau2 > 0 (a probability is never below 0); the
+  // device state is not known here without a synchronisation
   return step_impl(c, p, d_tokens, const_cast<int32_t*>(d_block_start), d_block_steps, d_flags,
-                   d_n_masked, d_stats, 0, nullptr, static_cast<hipStream_t>(stream));
+                   d_n_masked, d_stats, 0, nullptr, p->tau2 > 0.f, static_cast<hipStream_t>(stream));
 }
+
+namespace {
+
+// Whether the coming step needs the shadow block: tau2 > 0 and some sequence
+// may verify (next_verify, written by the decision kernel or the probe).
+bool need_shadow(const wino_params* p, const int32_t* h_next_verify) {
+  if (!(p->tau2 > 0.f)) return false;
+  for (int b = 0; b < p->batch; ++b)
+    if (h_next_verify[b]) return true;
+  return false;
+}
+
+}  // namespace
 
 wino_status wino_decode_block(wino_ctx* c, const wino_params* p, int32_t* d_tokens,
                               const int32_t* d_block_start, int32_t* h_steps, void* stream) {
@@ -460,11 +483,16 @@ wino_status wino_decode_block(wino_ctx* c, const wino_params* p, int32_t* d_toke
   const int B = p->batch;
   const int cap = p->max_steps > 0 ? p->max_steps : p->block_len;
   HIP_TRY(c, hipMemsetAsync(c->block_steps(), 0, sizeof(int32_t) * 2 * c->max_batch, st));
+  int32_t* h_nv = c->h_pinned + 2 * B;  // next_verify per sequence
+  HIP_TRY(c, launch_probe_verify(make_geom(p, d_block_start), d_tokens, c->next_verify(), st));
+  HIP_TRY(c, hipMemcpyAsync(h_nv, c->next_verify(), sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
+  HIP_TRY(c, hipStreamSynchronize(st));
   for (int it = 0;; ++it) {
     s = step_impl(c, p, d_tokens, const_cast<int32_t*>(d_block_start), c->block_steps(), nullptr,
-                  c->n_masked(), nullptr, 0, c->seq_steps(), st);
+                  c->n_masked(), nullptr, 0, c->seq_steps(), need_shadow(p, h_nv), st);
     if (s != WINO_OK) return s;
     HIP_TRY(c, hipMemcpyAsync(c->h_pinned, c->n_masked(), sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
+    HIP_TRY(c, hipMemcpyAsync(h_nv, c->next_verify(), sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
     HIP_TRY(c, hipStreamSynchronize(st));
     bool any = false;
     for (int b = 0; b < B; ++b) any |= c->h_pinned[b] > 0;
@@ -489,6 +517,9 @@ wino_status wino_decode(wino_ctx* c, const wino_params* p, int32_t* d_tokens, in
   const long max_forwards = (long)(p->gen_len / p->block_len) * cap;
   HIP_TRY(c, hipMemsetAsync(c->block_steps(), 0, sizeof(int32_t) * 2 * c->max_batch, st));
   int forwards = 0;
+  int32_t* h_nv = c->h_pinned + 2 * B;  // next_verify per sequence
+  HIP_TRY(c, launch_probe_verify(make_geom(p, d_block_start), d_tokens, c->next_verify(), st));
+  HIP_TRY(c, hipMemcpyAsync(h_nv, c->next_verify(), sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
   HIP_TRY(c, hipMemcpyAsync(c->h_pinned, d_block_start, sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
   HIP_TRY(c, hipStreamSynchronize(st));
   for (;;) {
@@ -500,12 +531,13 @@ wino_status wino_decode(wino_ctx* c, const wino_params* p, int32_t* d_tokens, in
       return WINO_ERR_STEP_CAP;
     }
     s = step_impl(c, p, d_tokens, d_block_start, c->block_steps(), nullptr, c->n_masked(), nullptr, 1,
-                  c->seq_steps(), st);
+                  c->seq_steps(), need_shadow(p, h_nv), st);
     if (s != WINO_OK) return s;
     ++forwards;
     HIP_TRY(c, hipMemcpyAsync(c->h_pinned, d_block_start, sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
     HIP_TRY(c, hipMemcpyAsync(c->h_pinned + B, c->block_steps(), sizeof(int32_t) * B,
                               hipMemcpyDeviceToHost, st));
+    HIP_TRY(c, hipMemcpyAsync(h_nv, c->next_verify(), sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
     HIP_TRY(c, hipStreamSynchronize(st));
     if (p->flags & WINO_FLAG_NO_CAP_FILL)
       for (int b = 0; b < B; ++b)
