@@ -14,6 +14,11 @@ Paper passages followed:
   row's probability of the current token, p(y_shad,l = y_cur,l), is < tau2.
 * Sec. 4.2.3, Eq. 4: both rules read the previous state y^(k-1) and act in one
   forward; iterate until Y_cur has no mask token.
+* Sec. 3 and the comparison with naive parallel sampling (Sec. 5): the
+  baselines unmask a fixed number M of tokens per step - the M most confident
+  masked positions of the block, M = 1 being Eq. 1 - with no threshold and no
+  verification (``tokens_per_step`` > 0 selects this mode; it needs no step
+  cap, a block takes ceil(L_b / M) steps).
 
 Readings of points the paper leaves open (each is a parameter or flag):
 * decoding is greedy (argmax, temperature 1, no sampling noise);
@@ -51,6 +56,7 @@ class Params:
     max_steps: int = 0        # per block; 0 -> block_len
     force_top1: bool = True
     cap_fill: bool = True
+    tokens_per_step: int = 0  # > 0: baseline decoding, M tokens per step (Sec. 3)
 
     @property
     def cap(self) -> int:
@@ -108,6 +114,21 @@ def wino_update(cur, conf, yhat, s, mask_id, tau1, tau2, force_top1=True, cap_no
     return new, flags
 
 
+def topm_update(cur, conf, yhat, mask_id, m):
+    """Baseline step (Sec. 3): unmask the m most confident masked positions of
+    the block (Eq. 1 for m = 1, naive parallel sampling for m > 1); equal
+    confidences go to the lower position.  Returns (new block, flags)."""
+    cur = np.asarray(cur, dtype=np.int64)
+    masked = np.flatnonzero(cur == mask_id)
+    order = masked[np.argsort(-np.asarray(conf, dtype=np.float64)[masked], kind="stable")]
+    pick = order[:m]
+    flags = np.full(cur.shape, KEEP, dtype=np.int64)
+    flags[pick] = DRAFT
+    new = cur.copy()
+    new[pick] = np.asarray(yhat)[pick]
+    return new, flags
+
+
 class ModelProvider:
     """Probabilities for Eq. 4 from the synthetic backbone (one sequence)."""
 
@@ -147,11 +168,20 @@ def step(provider, tokens, prm: Params, block_start: int, block_steps: int) -> S
     cur_for_verify = np.where(cur == prm.mask_id, 0, cur)
     s = verify_stats(z_sh, cur_for_verify)
     cap_now = prm.cap_fill and (block_steps + 1 >= prm.cap)
-    new, flags = wino_update(cur, conf, yhat, s, prm.mask_id, prm.tau1, prm.tau2,
-                             prm.force_top1, cap_now)
-    tokens[c0:c0 + prm.block_len] = new
     masked = cur == prm.mask_id
-    margin = np.where(masked, np.abs(conf - prm.tau1), np.abs(s - prm.tau2))
+    if prm.tokens_per_step > 0:
+        # the fixed schedule ends a block in ceil(L_b / M) <= L_b steps: no cap
+        new, flags = topm_update(cur, conf, yhat, prm.mask_id, prm.tokens_per_step)
+        # the selection flips only if the M-th and (M+1)-th confidences swap
+        c = np.sort(conf[masked])[::-1]
+        m = prm.tokens_per_step
+        half_gap = (c[m - 1] - c[m]) / 2 if len(c) > m else np.inf
+        margin = np.where(masked, half_gap, np.inf)
+    else:
+        new, flags = wino_update(cur, conf, yhat, s, prm.mask_id, prm.tau1, prm.tau2,
+                                 prm.force_top1, cap_now)
+        margin = np.where(masked, np.abs(conf - prm.tau1), np.abs(s - prm.tau2))
+    tokens[c0:c0 + prm.block_len] = new
     p = softmax_rows(z_cur)
     p[:, prm.mask_id] = -1.0
     top = np.sort(p, axis=-1)

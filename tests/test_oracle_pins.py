@@ -307,6 +307,73 @@ def test_greedy_special_case_equals_eq1_decoding(variant):
     assert out.tolist() == tok.tolist()
 
 
+def naive_parallel_reference(w, cfg, tok0, p, g, lb, m):
+    """Sec. 3 baseline written out independently: per step, a plain
+    bidirectional forward over Y (no shadow block), then the m masked
+    positions of the block with the highest top probability (over ids other
+    than the mask; equal values -> lower position) take their argmax id."""
+    tok = np.asarray(tok0, dtype=np.int64).copy()
+    s = p + g
+    steps = []
+    for b in range(g // lb):
+        n = 0
+        while any(tok[p + b * lb + l] == cfg.mask_id for l in range(lb)):
+            h = M.forward_hidden(w, cfg, tok, np.arange(s), np.ones((s, s), bool))
+            z = M.lm_logits(w, h[p + b * lb: p + (b + 1) * lb])
+            pr = np.exp(z - z.max(-1, keepdims=True))
+            pr /= pr.sum(-1, keepdims=True)
+            pr[:, cfg.mask_id] = 0.0
+            best = pr.max(-1)
+            cand = [l for l in range(lb) if tok[p + b * lb + l] == cfg.mask_id]
+            for l in sorted(cand, key=lambda l: (-best[l], l))[:m]:
+                tok[p + b * lb + l] = int(np.argmax(pr[l]))
+            n += 1
+        steps.append(n)
+    return tok, steps
+
+
+@pytest.mark.parametrize("m", [1, 3, 4, 9])
+def test_fixed_tokens_per_step_baseline(m):
+    """tokens_per_step = m: ceil(lb / m) steps per block, tokens equal to the
+    independently written baseline (m = 1 is Eq. 1 greedy decoding; m >= lb
+    is the full-parallel special case)."""
+    cfg = tiny_cfg()
+    w = wi.model_weights(cfg, seed=1, lm_head_std=wi.wide_lm_head_std(cfg))
+    p, g, lb = 8, 16, 8
+    prompt = wi.prompts(cfg, 1, p, seed=5)[0].numpy()
+    tok0 = np.concatenate([prompt, np.full(g, cfg.mask_id)]).astype(np.int64)
+    prm = W.Params(p, g, lb, cfg.mask_id, tokens_per_step=m)
+    trace = []
+    out, steps = W.decode(W.ModelProvider(w, cfg), tok0, prm, trace)
+    assert steps == [-(-lb // m)] * (g // lb)
+    # every step drafts exactly min(m, masks left in the block)
+    left = lb
+    for r in trace:
+        assert int((r.flags == W.DRAFT).sum()) == min(m, left)
+        left -= min(m, left)
+        left = left or lb
+    ref, ref_steps = naive_parallel_reference(w, cfg, tok0, p, g, lb, m)
+    assert steps == ref_steps
+    assert out.tolist() == ref.tolist()
+    # no position is ever re-masked or forced in this mode
+    assert all(not np.any((r.flags == W.REMASK) | (r.flags == W.FORCED)) for r in trace)
+
+
+def test_topm_selection_hand_worked():
+    """Five positions, mask id 9: masked 0, 2, 3, 4 with confidences 0.3, 0.9,
+    0.3, 0.5.  m = 2 drafts positions 2 and 4; m = 3 adds position 0 (tied
+    with 3, the lower position wins); m = 9 drafts every mask."""
+    cur = np.array([9, 5, 9, 9, 9])
+    conf = np.array([0.3, 0.99, 0.9, 0.3, 0.5])
+    yhat = np.array([10, 11, 12, 13, 14])
+    new, fl = W.topm_update(cur, conf, yhat, 9, 2)
+    assert fl.tolist() == [0, 0, 1, 0, 1] and new.tolist() == [9, 5, 12, 9, 14]
+    new, fl = W.topm_update(cur, conf, yhat, 9, 3)
+    assert fl.tolist() == [1, 0, 1, 0, 1] and new.tolist() == [10, 5, 12, 9, 14]
+    new, fl = W.topm_update(cur, conf, yhat, 9, 9)
+    assert fl.tolist() == [1, 0, 1, 1, 1] and new.tolist() == [10, 5, 12, 13, 14]
+
+
 def test_full_parallel_special_case_one_step_per_block(tiny_weights):
     """tau1 < 0 and tau2 = 0: every masked position clears tau1 at once."""
     cfg = tiny_cfg()
