@@ -88,12 +88,19 @@ typedef struct {
  * verifies (Eq. 3).  tau1 >= tau2 is accepted (tau2 = 0 disables verification,
  * the paper's only-draft ablation).  max_steps caps the steps one block may
  * take (0 = block_len); on the last allowed step verification is skipped and
- * every remaining mask is drafted, unless WINO_FLAG_NO_CAP_FILL is set. */
+ * every remaining mask is drafted, unless WINO_FLAG_NO_CAP_FILL is set.
+ * tokens_per_step > 0 selects the baseline decoders instead (Sec. 3): each
+ * step unmasks the tokens_per_step most confident masks of Y_cur (equal
+ * confidences: lower position first) - Eq. 1 greedy decoding for 1, naive
+ * parallel sampling above - with no threshold, no verification and no shadow
+ * block; a block then takes ceil(block_len / tokens_per_step) steps and
+ * tau1, tau2, max_steps and the flags are ignored. */
 typedef struct {
   int32_t batch, prompt_len, gen_len, block_len, mask_id;
   float tau1, tau2;
   int32_t max_steps;
   uint32_t flags;
+  int32_t tokens_per_step;
 } wino_params;
 
 /* Per block position diagnostics of one step. */
@@ -163,7 +170,8 @@ wino_status wino_decode(wino_ctx* ctx, const wino_params* p, int32_t* d_tokens,
  * materialised logits).  d_logits: bf16 [batch, 2*block_len, vocab]; rows
  * 0..block_len-1 are Y_cur, rows block_len..2*block_len-1 Y_shad.
  * d_cur_tokens int32 [batch, block_len] is updated in place by Eq. 4 (forced
- * draft per the flags; no step cap).  d_mask_bitmap uint8 [batch, block_len]
+ * draft per the flags; no step cap), or by the baseline rule when
+ * p->tokens_per_step > 0 (shadow rows unused).  d_mask_bitmap uint8 [batch, block_len]
  * receives 1 where the token is the mask after the step.  d_flags / d_stats
  * may be NULL.  d_workspace must hold wino_epilogue_workspace_bytes(...). */
 size_t wino_epilogue_workspace_bytes(int32_t batch, int32_t block_len, int32_t vocab);

@@ -58,7 +58,8 @@ class wino_weights(C.Structure):
 class wino_params(C.Structure):
     _fields_ = [("batch", C.c_int32), ("prompt_len", C.c_int32), ("gen_len", C.c_int32),
                 ("block_len", C.c_int32), ("mask_id", C.c_int32), ("tau1", C.c_float),
-                ("tau2", C.c_float), ("max_steps", C.c_int32), ("flags", C.c_uint32)]
+                ("tau2", C.c_float), ("max_steps", C.c_int32), ("flags", C.c_uint32),
+                ("tokens_per_step", C.c_int32)]
 
 
 class wino_row_stats(C.Structure):
@@ -135,8 +136,9 @@ def _check(status, where, ctx=None):
 
 
 def make_params(batch, prompt_len, gen_len, block_len, mask_id, tau1=0.7, tau2=0.9,
-                max_steps=0, flags=0) -> wino_params:
-    return wino_params(batch, prompt_len, gen_len, block_len, mask_id, tau1, tau2, max_steps, flags)
+                max_steps=0, flags=0, tokens_per_step=0) -> wino_params:
+    return wino_params(batch, prompt_len, gen_len, block_len, mask_id, tau1, tau2, max_steps, flags,
+                       tokens_per_step)
 
 
 # ------------------------------------------------------------------ entry points

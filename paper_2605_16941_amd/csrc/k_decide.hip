@@ -121,11 +121,21 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
   __syncthreads();
 
   const int steps_before = (!a.standalone && a.block_steps) ? a.block_steps[b] : 0;
-  const bool cap_now = !a.standalone && a.cap_fill && (steps_before + 1 >= a.cap);
+  const bool cap_now = !a.standalone && a.cap_fill && a.topm == 0 && (steps_before + 1 >= a.cap);
   for (int l = tid; l < Lb; l += 256) {
     const bool masked = s_cur[l] == a.mask_id;
     int f = WINO_KEEP_FLAG;
-    if (masked) {
+    if (a.topm > 0) {
+      // baseline (Sec. 3): draft when fewer than topm masked positions rank
+      // above this one (higher confidence, or equal at a lower position)
+      if (masked) {
+        const float v = s_val[l];
+        int rank = 0;
+        for (int j = 0; j < Lb && rank < a.topm; ++j)
+          rank += s_cur[j] == a.mask_id && (s_val[j] > v || (s_val[j] == v && j < l));
+        if (rank < a.topm) { f = WINO_DRAFT_FLAG; s_any_draft = 1; }
+      }
+    } else if (masked) {
       if (cap_now) f = WINO_CAPFILL_FLAG;
       else if (s_val[l] > a.tau1) { f = WINO_DRAFT_FLAG; s_any_draft = 1; }
     } else if ((a.verify || a.standalone) && !cap_now && s_val[l] < a.tau2) {
@@ -134,7 +144,7 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
     s_flag[l] = f;
   }
   __syncthreads();
-  if (tid == 0 && !cap_now && a.force_top1 && s_nmask > 0 && !s_any_draft) {
+  if (tid == 0 && a.topm == 0 && !cap_now && a.force_top1 && s_nmask > 0 && !s_any_draft) {
     // Eq. 1: the most confident masked position (lowest position on ties)
     int best = -1;
     float bv = 0.f;

@@ -153,6 +153,7 @@ struct DecideArgs {
   int32_t* n_masked;     // [B] or null
   void* stats;           // wino_row_stats [B, Lb] or null
   int verify;            // shadow rows were computed: the Eq. 3 rule applies
+  int topm;              // > 0: baseline mode, draft the topm most confident masks
   // [B] or null: 1 if the sequence's next step may verify (it is active and
   // its next Y_cur holds both a mask and a drafted token), else 0
   int32_t* next_verify;

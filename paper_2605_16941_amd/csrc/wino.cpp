@@ -160,7 +160,7 @@ bool shape_supported(const wino_model_config& c) {
 wino_status validate_params(wino_ctx* ctx, const wino_params* p) {
   if (!p) return WINO_ERR_INVALID_ARG;
   if (!std::isfinite(p->tau1) || !std::isfinite(p->tau2)) return WINO_ERR_INVALID_ARG;
-  if (p->max_steps < 0) return WINO_ERR_INVALID_ARG;
+  if (p->max_steps < 0 || p->tokens_per_step < 0) return WINO_ERR_INVALID_ARG;
   if (p->batch < 1 || p->prompt_len < 0 || p->gen_len < 1 || p->block_len < 1) return WINO_ERR_SHAPE;
   if (p->block_len > p->gen_len || p->gen_len % p->block_len) return WINO_ERR_SHAPE;
   if (p->block_len > 4096) return WINO_ERR_SHAPE;
@@ -301,6 +301,7 @@ wino_status step_impl(wino_ctx* c, const wino_params* p, int32_t* tokens, int32_
                       int32_t* block_steps, uint8_t* flags, int32_t* n_masked, void* stats,
                       int advance, int32_t* seq_steps, bool shadow, hipStream_t st) {
   const wino_model_config& m = c->cfg;
+  shadow = shadow && p->tokens_per_step == 0;  // the baselines never verify
   const StepGeom g = make_geom(p, block_start, shadow);
   wino_status s = run_forward(c, g, tokens, 2 * m.n_layers, st);
   if (s != WINO_OK) return s;
@@ -341,6 +342,7 @@ wino_status step_impl(wino_ctx* c, const wino_params* p, int32_t* tokens, int32_
   da.seq_steps = seq_steps; da.flags = flags; da.bitmap = nullptr; da.n_masked = n_masked;
   da.stats = stats;
   da.verify = shadow;
+  da.topm = p->tokens_per_step;
   da.next_verify = c->next_verify();
   {
     Bracket br(c, K_DECIDE, st);
@@ -462,10 +464,16 @@ wino_status wino_step(wino_ctx* c, const wino_params* p, int32_t* d_tokens,
 
 namespace {
 
+// Steps one block may take: the cap, or the fixed schedule of the baselines.
+int block_cap(const wino_params* p) {
+  if (p->tokens_per_step > 0) return (p->block_len + p->tokens_per_step - 1) / p->tokens_per_step;
+  return p->max_steps > 0 ? p->max_steps : p->block_len;
+}
+
 // Whether the coming step needs the shadow block: tau2 > 0 and some sequence
 // may verify (next_verify, written by the decision kernel or the probe).
 bool need_shadow(const wino_params* p, const int32_t* h_next_verify) {
-  if (!(p->tau2 > 0.f)) return false;
+  if (!(p->tau2 > 0.f) || p->tokens_per_step > 0) return false;
   for (int b = 0; b < p->batch; ++b)
     if (h_next_verify[b]) return true;
   return false;
@@ -481,7 +489,7 @@ wino_status wino_decode_block(wino_ctx* c, const wino_params* p, int32_t* d_toke
   if (!d_tokens || !d_block_start) return WINO_ERR_INVALID_ARG;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int B = p->batch;
-  const int cap = p->max_steps > 0 ? p->max_steps : p->block_len;
+  const int cap = block_cap(p);
   HIP_TRY(c, hipMemsetAsync(c->block_steps(), 0, sizeof(int32_t) * 2 * c->max_batch, st));
   int32_t* h_nv = c->h_pinned + 2 * B;  // next_verify per sequence
   HIP_TRY(c, launch_probe_verify(make_geom(p, d_block_start), d_tokens, c->next_verify(), st));
@@ -513,7 +521,7 @@ wino_status wino_decode(wino_ctx* c, const wino_params* p, int32_t* d_tokens, in
   if (!d_tokens || !d_block_start) return WINO_ERR_INVALID_ARG;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int B = p->batch;
-  const int cap = p->max_steps > 0 ? p->max_steps : p->block_len;
+  const int cap = block_cap(p);
   const long max_forwards = (long)(p->gen_len / p->block_len) * cap;
   HIP_TRY(c, hipMemsetAsync(c->block_steps(), 0, sizeof(int32_t) * 2 * c->max_batch, st));
   int forwards = 0;
@@ -539,7 +547,7 @@ wino_status wino_decode(wino_ctx* c, const wino_params* p, int32_t* d_tokens, in
                               hipMemcpyDeviceToHost, st));
     HIP_TRY(c, hipMemcpyAsync(h_nv, c->next_verify(), sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
     HIP_TRY(c, hipStreamSynchronize(st));
-    if (p->flags & WINO_FLAG_NO_CAP_FILL)
+    if ((p->flags & WINO_FLAG_NO_CAP_FILL) && p->tokens_per_step == 0)
       for (int b = 0; b < B; ++b)
         if (c->h_pinned[b] < p->gen_len && c->h_pinned[B + b] >= cap) {
           c->err = "block did not finish within its step cap";
@@ -563,6 +571,7 @@ wino_status wino_epilogue(const wino_params* p, int32_t vocab, const void* d_log
                           void* d_workspace, size_t workspace_bytes, void* stream) {
   if (!p || !d_logits || !d_cur_tokens || !d_mask_bitmap || !d_workspace) return WINO_ERR_INVALID_ARG;
   if (!std::isfinite(p->tau1) || !std::isfinite(p->tau2)) return WINO_ERR_INVALID_ARG;
+  if (p->tokens_per_step < 0) return WINO_ERR_INVALID_ARG;
   if (p->batch < 1 || p->block_len < 1 || vocab < 8 || vocab % 8) return WINO_ERR_SHAPE;
   if (p->mask_id < 0 || p->mask_id >= vocab) return WINO_ERR_INVALID_ARG;
   const size_t need = wino_epilogue_workspace_bytes(p->batch, p->block_len, vocab);
@@ -585,6 +594,7 @@ wino_status wino_epilogue(const wino_params* p, int32_t vocab, const void* d_log
   da.tau1 = p->tau1; da.tau2 = p->tau2;
   da.force_top1 = !(p->flags & WINO_FLAG_NO_FORCE_TOP1);
   da.cap_fill = 0; da.cap = 0;
+  da.topm = p->tokens_per_step;
   da.standalone = 1;
   da.tokens = d_cur_tokens;
   da.flags = d_flags; da.bitmap = d_mask_bitmap; da.stats = d_stats;
