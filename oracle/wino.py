@@ -14,6 +14,8 @@ Paper passages followed:
   row's probability of the current token, p(y_shad,l = y_cur,l), is < tau2.
 * Sec. 4.2.3, Eq. 4: both rules read the previous state y^(k-1) and act in one
   forward; iterate until Y_cur has no mask token.
+* Sec. 4.3: a position's finalization step is the first step from which its
+  token no longer changes (the WINO+ trajectory data).
 * Sec. 3 and the comparison with naive parallel sampling (Sec. 5): the
   baselines unmask a fixed number M of tokens per step - the M most confident
   masked positions of the block, M = 1 being Eq. 1 - with no threshold and no
@@ -204,6 +206,22 @@ def decode_block(provider, tokens, prm: Params, block_start: int, trace=None):
             return tokens, steps
         if prm.cap_fill is False and steps >= prm.cap:
             return tokens, steps
+
+
+def finalization_steps(states, prompt_len: int) -> np.ndarray:
+    """Sec. 4.3 (verified trajectories): for the states Y^(0..K) of one
+    sequence's decode, t_l = min{t : y_l^(j) = y_l^(K) for every j >= t};
+    prompt positions get 0.  Written from the definition: scan t upward."""
+    Y = np.asarray(states, dtype=np.int64)          # [K + 1, P + G]
+    K = Y.shape[0] - 1
+    final = Y[K]
+    t = np.zeros(Y.shape[1], dtype=np.int64)
+    for l in range(prompt_len, Y.shape[1]):
+        for cand in range(K + 1):
+            if np.all(Y[cand:, l] == final[l]):
+                t[l] = cand
+                break
+    return t
 
 
 def decode(provider, tokens, prm: Params, trace=None):

@@ -374,6 +374,43 @@ def test_topm_selection_hand_worked():
     assert fl.tolist() == [1, 0, 1, 1, 1] and new.tolist() == [10, 5, 12, 13, 14]
 
 
+def test_finalization_steps_hand_worked():
+    """Prompt of 1 and 4 response positions (mask 9) over K = 4 steps:
+    position 1 drafted at step 1 and kept (t = 1); position 2 drafted at 1,
+    re-masked at 2, drafted again with the same id at 3 (t = 3); position 3
+    drafted 7 at 2, re-masked at 3, drafted 6 at 4 (t = 4); position 4
+    drafted at 4 (t = 4)."""
+    Y = [[5, 9, 9, 9, 9],
+         [5, 1, 2, 9, 9],
+         [5, 1, 9, 7, 9],
+         [5, 1, 2, 9, 9],
+         [5, 1, 2, 6, 4]]
+    assert W.finalization_steps(Y, 1).tolist() == [0, 1, 3, 4, 4]
+
+
+def test_finalization_steps_of_a_decode(tiny_weights):
+    """Along a real decode: t_l is the last step at which position l changed,
+    every response position gets 1 <= t_l <= K, and each block's positions
+    finalise within that block's steps."""
+    cfg = tiny_cfg()
+    p, g, lb = 8, 16, 8
+    tok0 = np.concatenate([wi.prompts(cfg, 1, p, seed=4)[0].numpy(), np.full(g, cfg.mask_id)])
+    prm = W.Params(p, g, lb, cfg.mask_id, tau1=0.3, tau2=0.9)
+    trace = []
+    out, steps = W.decode(W.ModelProvider(tiny_weights, cfg), tok0, prm, trace)
+    states = [tok0] + [r.tokens for r in trace]
+    t = W.finalization_steps(states, p)
+    K = len(trace)
+    assert np.all(t[:p] == 0) and np.all((t[p:] >= 1) & (t[p:] <= K))
+    for l in range(p, p + g):
+        changes = [k for k in range(1, K + 1) if states[k][l] != states[k - 1][l]]
+        assert t[l] == changes[-1]
+    ends = np.cumsum(steps)
+    for b in range(g // lb):
+        lo = ends[b - 1] if b else 0
+        assert np.all((t[p + b * lb:p + (b + 1) * lb] > lo) & (t[p + b * lb:p + (b + 1) * lb] <= ends[b]))
+
+
 def test_full_parallel_special_case_one_step_per_block(tiny_weights):
     """tau1 < 0 and tau2 = 0: every masked position clears tau1 at once."""
     cfg = tiny_cfg()
