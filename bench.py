@@ -126,6 +126,34 @@ def run_workload(P, wi, cfg, weights, name, steps, warmup, profile_dominant=True
                        "steps_per_seq_mean": sum(seq_steps) / len(seq_steps)}}
 
 
+def run_baselines(P, wi, cfg, weights, name, ms=(1, 4)):
+    """Full decodes from the prompt with the Sec. 3 baselines (tokens_per_step
+    m: 1 = Eq. 1 greedy, m > 1 naive parallel sampling) on the same kernels,
+    next to WINO: forwards, tokens/s and WINO's step reduction / speedup."""
+    import torch
+    preset, B, p, g, lb, tau1, tau2, img = CONFIGS[name]
+    model = P.WinoModel(cfg, weights, B, p + g + lb)
+    out = {}
+    for label, m in [("wino", 0)] + [(f"tokens_per_step_{m}", m) for m in ms]:
+        prm = P.make_params(B, p, g, lb, cfg.mask_id, tau1, tau2, tokens_per_step=m)
+        tok = wi.initial_tokens(wi.prompts(cfg, B, p, seed=1000, image_prefix=img), g, cfg.mask_id).cuda()
+        bs = torch.zeros(B, dtype=torch.int32, device="cuda")
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        _, forwards = P.wino_decode(model.ctx, prm, tok, bs)
+        torch.cuda.synchronize()
+        sec = time.perf_counter() - t0
+        out[label] = {"forwards": forwards, "seconds": round(sec, 4), "tokens_per_s": round(B * g / sec, 2)}
+    model.close()
+    w = out["wino"]
+    for m in ms:
+        b = out[f"tokens_per_step_{m}"]
+        b["wino_step_reduction"] = round(b["forwards"] / w["forwards"], 3)
+        b["wino_tps_speedup"] = round(w["tokens_per_s"] / b["tokens_per_s"], 3)
+    out["workload"] = f"{preset} decode, batch {B}, prompt {p}, gen {g}, block {lb}, tau1 {tau1}, tau2 {tau2}"
+    return out
+
+
 def cpu_baseline(wi, cfg, weights, name):
     """The float64 oracle on a bounded sample: one layer of one sequence plus
     the LM head of its block rows, extrapolated to a full batched step."""
@@ -251,6 +279,9 @@ def main():
         line["bs1"] = {"steps_per_s": round(1e3 / ms1, 3), "ms_per_step": round(ms1, 3),
                        "tokens_per_s": r1["decode"]["tokens_per_s"], "decode": r1["decode"],
                        "kernels": r1["kernels"]}
+    if a.config == "bs16" and not a.no_bs1:
+        log("baseline decoders (bs1)")
+        line["baselines"] = run_baselines(P, wi, cfg, weights, "bs1")
     if not a.no_cpu_baseline:
         log("cpu baseline (oracle sample)")
         line["cpu_baseline"] = cpu_baseline(wi, cfg, weights, a.config)

@@ -151,19 +151,26 @@ wino_status wino_step(wino_ctx* ctx, const wino_params* p, int32_t* d_tokens,
                       int32_t* d_n_masked, wino_row_stats* d_stats, void* stream);
 
 /* Iterate wino_step on the current block of every sequence until none holds a
- * mask (Sec. 4.2.3).  h_steps [batch] receives the steps each sequence took.
- * Synchronises `stream` once per step. */
+ * mask (Sec. 4.2.3).  d_final_step int32 [batch, gen_len] (device, or NULL)
+ * is written as in wino_decode.  h_steps [batch] receives the steps each
+ * sequence took.  Synchronises `stream` once per step. */
 wino_status wino_decode_block(wino_ctx* ctx, const wino_params* p, int32_t* d_tokens,
-                              const int32_t* d_block_start, int32_t* h_steps, void* stream);
+                              const int32_t* d_block_start, int32_t* d_final_step,
+                              int32_t* h_steps, void* stream);
 
 /* Full semi-autoregressive decode (Sec. 3): every sequence advances to its
  * next block as soon as its current block holds no mask; returns when all
  * sequences reach gen_len.  Resumable: d_block_start [batch] gives each
- * sequence's starting block and ends at gen_len.  h_steps_per_seq [batch]
- * (or NULL) receives the steps each sequence took; h_forward_passes (or NULL)
- * the number of batched forwards.  Synchronises once per step. */
+ * sequence's starting block and ends at gen_len.  d_final_step int32
+ * [batch, gen_len] (device, or NULL) receives, for every response position
+ * this call changes, the sequence's step (1-based, counted from this call)
+ * at which the position last changed: from an all-mask response that is the
+ * finalization step t_l of Sec. 4.3; positions never changed keep the
+ * caller's values.  h_steps_per_seq [batch] (or NULL) receives the steps
+ * each sequence took; h_forward_passes (or NULL) the number of batched
+ * forwards.  Synchronises once per step. */
 wino_status wino_decode(wino_ctx* ctx, const wino_params* p, int32_t* d_tokens,
-                        int32_t* d_block_start, int32_t* h_steps_per_seq,
+                        int32_t* d_block_start, int32_t* d_final_step, int32_t* h_steps_per_seq,
                         int32_t* h_forward_passes, void* stream);
 
 /* Standalone decision from given bf16 logits (the fused step's epilogue on

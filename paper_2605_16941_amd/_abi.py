@@ -76,8 +76,8 @@ _protos = {
     "wino_destroy": (_i32, [_vp]),
     "wino_workspace_bytes": (_sz, [_P(wino_model_config), _i32, _i32]),
     "wino_step": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
-    "wino_decode_block": (_i32, [_vp, _P(wino_params), _vp, _vp, _P(_i32), _vp]),
-    "wino_decode": (_i32, [_vp, _P(wino_params), _vp, _vp, _P(_i32), _P(_i32), _vp]),
+    "wino_decode_block": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _P(_i32), _vp]),
+    "wino_decode": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _P(_i32), _P(_i32), _vp]),
     "wino_epilogue_workspace_bytes": (_sz, [_i32, _i32, _i32]),
     "wino_epilogue": (_i32, [_P(wino_params), _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "wino_debug_logits": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _vp]),
@@ -167,22 +167,26 @@ def wino_step(ctx, p: wino_params, tokens, block_start, block_steps=None, flags=
                          _ptr(stats, None, "stats"), _stream(stream)), "wino_step", ctx)
 
 
-def wino_decode_block(ctx, p: wino_params, tokens, block_start, stream=None):
+def wino_decode_block(ctx, p: wino_params, tokens, block_start, final_step=None, stream=None):
+    """Returns the per-sequence steps.  final_step as in wino_decode."""
     import torch
     steps = (C.c_int32 * p.batch)()
+    fs = _ptr(final_step, torch.int32, "final_step") if final_step is not None else None
     _check(lib.wino_decode_block(ctx, C.byref(p), _ptr(tokens, torch.int32, "tokens"),
-                                 _ptr(block_start, torch.int32, "block_start"), steps,
+                                 _ptr(block_start, torch.int32, "block_start"), fs, steps,
                                  _stream(stream)), "wino_decode_block", ctx)
     return list(steps)
 
 
-def wino_decode(ctx, p: wino_params, tokens, block_start, stream=None):
-    """Returns (per-sequence steps, batched forward passes)."""
+def wino_decode(ctx, p: wino_params, tokens, block_start, final_step=None, stream=None):
+    """Returns (per-sequence steps, batched forward passes).  final_step: int32
+    [batch, gen_len] device tensor for the finalization steps, or None."""
     import torch
     steps = (C.c_int32 * p.batch)()
     fw = C.c_int32(0)
+    fs = _ptr(final_step, torch.int32, "final_step") if final_step is not None else None
     _check(lib.wino_decode(ctx, C.byref(p), _ptr(tokens, torch.int32, "tokens"),
-                           _ptr(block_start, torch.int32, "block_start"), steps, C.byref(fw),
+                           _ptr(block_start, torch.int32, "block_start"), fs, steps, C.byref(fw),
                            _stream(stream)), "wino_decode", ctx)
     return list(steps), fw.value
 

@@ -60,6 +60,7 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
   RowStats* stats = reinterpret_cast<RowStats*>(a.stats);
 
   int32_t* cur_ptr;
+  int32_t* fin_ptr = nullptr;  // finalization-step record of Y_cur, or null
   bool done = false;
   if (a.standalone) {
     cur_ptr = a.tokens + (size_t)b * Lb;
@@ -69,6 +70,7 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
     // same clamping as the forward kernels: Y_cur always lies inside the response
     const int bsc = bs < 0 ? 0 : (bs > a.G - Lb ? a.G - Lb : bs);
     cur_ptr = a.tokens + (size_t)b * a.S + a.P + bsc;
+    if (a.final_step && a.seq_steps) fin_ptr = a.final_step + (size_t)b * a.G + bsc;
   }
   if (tid == 0) { s_nmask = 0; s_nmask_after = 0; s_any_draft = 0; s_forced = -1; }
   __syncthreads();
@@ -153,12 +155,16 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
     s_flag[best] = WINO_FORCED_FLAG;
   }
   __syncthreads();
+  const int step_no = fin_ptr ? a.seq_steps[b] + 1 : 0;
   for (int l = tid; l < Lb; l += 256) {
     const int f = s_flag[l];
     int t = s_cur[l];
     if (f == WINO_DRAFT_FLAG || f == WINO_FORCED_FLAG || f == WINO_CAPFILL_FLAG) t = s_hat[l];
     else if (f == WINO_REMASK_FLAG) t = a.mask_id;
-    if (t != s_cur[l]) cur_ptr[l] = t;
+    if (t != s_cur[l]) {
+      cur_ptr[l] = t;
+      if (fin_ptr) fin_ptr[l] = step_no;  // Sec. 4.3: last change = finalization
+    }
     if (t == a.mask_id) atomicAdd(&s_nmask_after, 1);
     if (a.flags) a.flags[(size_t)b * Lb + l] = (uint8_t)f;
     if (a.bitmap) a.bitmap[(size_t)b * Lb + l] = t == a.mask_id;

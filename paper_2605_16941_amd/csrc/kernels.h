@@ -154,6 +154,9 @@ struct DecideArgs {
   void* stats;           // wino_row_stats [B, Lb] or null
   int verify;            // shadow rows were computed: the Eq. 3 rule applies
   int topm;              // > 0: baseline mode, draft the topm most confident masks
+  // [B, G] or null: step number (seq_steps after this step) written at every
+  // response position the step changes (needs seq_steps)
+  int32_t* final_step;
   // [B] or null: 1 if the sequence's next step may verify (it is active and
   // its next Y_cur holds both a mask and a drafted token), else 0
   int32_t* next_verify;

@@ -299,7 +299,8 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
 // current rows then, so the result is unchanged.
 wino_status step_impl(wino_ctx* c, const wino_params* p, int32_t* tokens, int32_t* block_start,
                       int32_t* block_steps, uint8_t* flags, int32_t* n_masked, void* stats,
-                      int advance, int32_t* seq_steps, bool shadow, hipStream_t st) {
+                      int advance, int32_t* seq_steps, bool shadow, hipStream_t st,
+                      int32_t* final_step = nullptr) {
   const wino_model_config& m = c->cfg;
   shadow = shadow && p->tokens_per_step == 0;  // the baselines never verify
   const StepGeom g = make_geom(p, block_start, shadow);
@@ -343,6 +344,7 @@ wino_status step_impl(wino_ctx* c, const wino_params* p, int32_t* tokens, int32_
   da.stats = stats;
   da.verify = shadow;
   da.topm = p->tokens_per_step;
+  da.final_step = final_step;
   da.next_verify = c->next_verify();
   {
     Bracket br(c, K_DECIDE, st);
@@ -482,7 +484,8 @@ bool need_shadow(const wino_params* p, const int32_t* h_next_verify) {
 }  // namespace
 
 wino_status wino_decode_block(wino_ctx* c, const wino_params* p, int32_t* d_tokens,
-                              const int32_t* d_block_start, int32_t* h_steps, void* stream) {
+                              const int32_t* d_block_start, int32_t* d_final_step, int32_t* h_steps,
+                              void* stream) {
   if (!c) return WINO_ERR_INVALID_ARG;
   wino_status s = validate_params(c, p);
   if (s != WINO_OK) return s;
@@ -497,7 +500,7 @@ wino_status wino_decode_block(wino_ctx* c, const wino_params* p, int32_t* d_toke
   HIP_TRY(c, hipStreamSynchronize(st));
   for (int it = 0;; ++it) {
     s = step_impl(c, p, d_tokens, const_cast<int32_t*>(d_block_start), c->block_steps(), nullptr,
-                  c->n_masked(), nullptr, 0, c->seq_steps(), need_shadow(p, h_nv), st);
+                  c->n_masked(), nullptr, 0, c->seq_steps(), need_shadow(p, h_nv), st, d_final_step);
     if (s != WINO_OK) return s;
     HIP_TRY(c, hipMemcpyAsync(c->h_pinned, c->n_masked(), sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
     HIP_TRY(c, hipMemcpyAsync(h_nv, c->next_verify(), sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
@@ -514,7 +517,8 @@ wino_status wino_decode_block(wino_ctx* c, const wino_params* p, int32_t* d_toke
 }
 
 wino_status wino_decode(wino_ctx* c, const wino_params* p, int32_t* d_tokens, int32_t* d_block_start,
-                        int32_t* h_steps_per_seq, int32_t* h_forward_passes, void* stream) {
+                        int32_t* d_final_step, int32_t* h_steps_per_seq, int32_t* h_forward_passes,
+                        void* stream) {
   if (!c) return WINO_ERR_INVALID_ARG;
   wino_status s = validate_params(c, p);
   if (s != WINO_OK) return s;
@@ -539,7 +543,7 @@ wino_status wino_decode(wino_ctx* c, const wino_params* p, int32_t* d_tokens, in
       return WINO_ERR_STEP_CAP;
     }
     s = step_impl(c, p, d_tokens, d_block_start, c->block_steps(), nullptr, c->n_masked(), nullptr, 1,
-                  c->seq_steps(), need_shadow(p, h_nv), st);
+                  c->seq_steps(), need_shadow(p, h_nv), st, d_final_step);
     if (s != WINO_OK) return s;
     ++forwards;
     HIP_TRY(c, hipMemcpyAsync(c->h_pinned, d_block_start, sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));

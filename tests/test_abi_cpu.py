@@ -85,8 +85,8 @@ def test_create_rejects_bad_arguments_before_gpu_work(abi):
 def test_entry_points_reject_null_context_and_bad_params(abi):
     p = abi.make_params(1, 32, 64, 16, 4095)
     assert abi.lib.wino_step(None, C.byref(p), None, None, None, None, None, None, None) == -1
-    assert abi.lib.wino_decode(None, C.byref(p), None, None, None, None, None) == -1
-    assert abi.lib.wino_decode_block(None, C.byref(p), None, None, None, None) == -1
+    assert abi.lib.wino_decode(None, C.byref(p), None, None, None, None, None, None) == -1
+    assert abi.lib.wino_decode_block(None, C.byref(p), None, None, None, None, None) == -1
     assert abi.lib.wino_destroy(None) == -1
     assert abi.lib.wino_profile(None, 1) == -1
     # standalone epilogue: host-side validation

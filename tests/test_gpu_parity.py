@@ -299,9 +299,11 @@ def test_decode_matches_oracle(P, variant, tau1, tau2, lb):
     tok0 = batch_tokens(cfg, B, p, g, seed=9)
     tok = torch.tensor(tok0, dtype=torch.int32, device="cuda")
     bs = torch.zeros(B, dtype=torch.int32, device="cuda")
-    steps, forwards = P.wino_decode(model.ctx, prm_c, tok, bs)
+    fin = torch.zeros(B, g, dtype=torch.int32, device="cuda")
+    steps, forwards = P.wino_decode(model.ctx, prm_c, tok, bs, fin)
     torch.cuda.synchronize()
     got = tok.cpu().numpy()
+    fin = fin.cpu().numpy()
     assert np.all(bs.cpu().numpy() == g)
     assert not np.any(got[:, p:] == cfg.mask_id)
     assert np.array_equal(got[:, :p], tok0[:, :p])
@@ -315,6 +317,10 @@ def test_decode_matches_oracle(P, variant, tau1, tau2, lb):
         if robust:
             assert np.array_equal(got[b], final), f"seq {b}: decoded tokens differ"
             assert steps[b] == len(traj)
+            # Sec. 4.3 finalization steps, from the oracle's states Y^(0..K)
+            t = W.finalization_steps([tok0[b]] + [r.tokens for (_, _, _, r) in traj], p)
+            assert np.array_equal(fin[b], t[p:]), f"seq {b}: finalization steps differ"
+        assert np.all((fin[b] >= 1) & (fin[b] <= steps[b]))
     model.close()
 
 
@@ -376,9 +382,11 @@ def test_decode_block_matches_oracle(P, mixed):
         tok0[1, p:p + lb][rng.random(lb) < 0.5] = cfg.mask_id
     tok = torch.tensor(tok0, dtype=torch.int32, device="cuda")
     bs = torch.tensor(starts, dtype=torch.int32, device="cuda")
-    steps = P.wino_decode_block(model.ctx, prm_c, tok, bs)
+    fin = torch.zeros(B, g, dtype=torch.int32, device="cuda")
+    steps = P.wino_decode_block(model.ctx, prm_c, tok, bs, fin)
     torch.cuda.synchronize()
     got = tok.cpu().numpy()
+    fin = fin.cpu().numpy()
     prov = W.ModelProvider(w, cfg, act_round=M.round_bf16)
     n_cmp = 0
     for b in range(B):
@@ -391,6 +399,10 @@ def test_decode_block_matches_oracle(P, mixed):
         if robust_trajectory(traj, p, lb, cfg.mask_id):
             assert np.array_equal(got[b], final), f"seq {b}: block differs from the oracle"
             assert steps[b] == len(traj)
+            # Sec. 4.3 finalization steps relative to this call (0: never changed,
+            # e.g. a kept pre-filled draft); re-masked drafts finalise later
+            t = W.finalization_steps([tok0[b]] + [r.tokens for (_, _, _, r) in traj], p)
+            assert np.array_equal(fin[b], t[p:]), f"seq {b}: finalization steps differ"
             n_cmp += 1
     assert n_cmp > 0
     model.close()
