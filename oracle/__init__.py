@@ -15,7 +15,9 @@ Everything is plain numpy in float64, computed straight from the definitions:
                  semi-autoregressive decode (Sec. 3).
 * ``epilogue`` - the decision taken directly from given logits of the current
                  and shadow blocks (the standalone epilogue workload).
+* ``losses``   - per-row entropy, target log-likelihood and greedy confidence
+                 of a WINO+ training state (Sec. 4.3).
 
 Readings of points the paper leaves open are stated where they are used.
 """
-from . import model, wino, epilogue  # noqa: F401
+from . import model, wino, epilogue, losses  # noqa: F401

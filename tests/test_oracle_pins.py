@@ -519,3 +519,55 @@ def test_norm_gain_scales_like_the_following_matrix(norm, mat):
     h_mat = M.forward_hidden(w, cfg, ext, pos, allowed)
     np.testing.assert_allclose(h_gain, h_mat, atol=1e-12)
     assert np.max(np.abs(h_gain - base)) > 1e-4
+
+
+# ---------------------------------------------------------------- WINO+ per-row quantities (Sec. 4.3)
+from oracle import losses as L  # noqa: E402
+
+
+def test_losses_uniform_and_two_point_closed_forms():
+    V = 50
+    e, nll, conf, yhat = L.row_quantities(np.zeros((1, V)), [7], mask_id=V - 1)
+    assert abs(e[0] - math.log(V)) < 1e-12 and abs(nll[0] - math.log(V)) < 1e-12
+    assert abs(conf[0] - 1.0 / V) < 1e-15 and yhat[0] == 0   # lowest id among ties
+    # two live ids (a, b), the rest at -1e4: binary entropy of q = sigmoid(a - b)
+    a, b = 1.3, -0.4
+    z = np.full((1, V), -1e4)
+    z[0, 3], z[0, 11] = a, b
+    q = 1.0 / (1.0 + math.exp(b - a))
+    e, nll, conf, yhat = L.row_quantities(z, [11], mask_id=V - 1)
+    assert abs(e[0] - (-q * math.log(q) - (1 - q) * math.log(1 - q))) < 1e-12
+    assert abs(nll[0] + math.log(1 - q)) < 1e-12
+    assert yhat[0] == 3 and abs(conf[0] - q) < 1e-12
+
+
+def test_losses_peaked_row_and_mask_excluded_from_prediction():
+    V = 40
+    z = np.zeros((2, V))
+    z[0, 5] = 60.0
+    z[1, V - 1] = 60.0          # the mask id dominates row 1
+    z[1, 9] = 3.0
+    e, nll, conf, yhat = L.row_quantities(z, [5, V - 1], mask_id=V - 1)
+    assert e[0] < 1e-20 and nll[0] < 1e-20 and yhat[0] == 5
+    assert yhat[1] == 9 and conf[1] < 1e-20 and nll[1] < 1e-20
+
+
+def test_losses_entropy_is_expected_nll_and_bounded():
+    rng = np.random.default_rng(3)
+    V = 64
+    z = rng.normal(0, 3, (4, V))
+    e, _, _, _ = L.row_quantities(z, np.zeros(4, dtype=int), mask_id=V - 1)
+    assert np.all(e >= 0) and np.all(e <= math.log(V) + 1e-12)
+    p = W.softmax_rows(z)
+    for r in range(4):
+        nll_all = L.row_quantities(np.repeat(z[r:r + 1], V, 0), np.arange(V), mask_id=V - 1)[1]
+        assert abs(float(p[r] @ nll_all) - e[r]) < 1e-10
+
+
+def test_training_state_reveals_tokens_finalized_before_t():
+    final = np.array([4, 4, 10, 11, 12, 13])
+    t_fin = np.array([0, 0, 2, 1, 3, 2])
+    assert L.training_state(final, t_fin, 1, 2, 99).tolist() == [4, 4, 99, 99, 99, 99]
+    assert L.training_state(final, t_fin, 2, 2, 99).tolist() == [4, 4, 99, 11, 99, 99]
+    assert L.training_state(final, t_fin, 3, 2, 99).tolist() == [4, 4, 10, 11, 99, 13]
+    assert L.training_state(final, t_fin, 4, 2, 99).tolist() == [4, 4, 10, 11, 12, 13]
