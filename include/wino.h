@@ -173,6 +173,25 @@ wino_status wino_decode(wino_ctx* ctx, const wino_params* p, int32_t* d_tokens,
                         int32_t* d_block_start, int32_t* d_final_step, int32_t* h_steps_per_seq,
                         int32_t* h_forward_passes, void* stream);
 
+/* Per response position quantities of a WINO+ training state (Sec. 4.3). */
+typedef struct {
+  float entropy;  /* H(p) = -sum_v p(v) log p(v), p = softmax of the row's logits */
+  float nll;      /* -log p(target)                                             */
+  float conf;     /* greedy confidence: max p over ids != mask_id               */
+  int32_t argmax; /* greedy prediction: lowest id reaching conf                 */
+} wino_row_loss;
+
+/* The forward half of the WINO+ objective (Sec. 4.3, Eq. 6-7): for each
+ * sequence, a plain bidirectional forward over the training state d_tokens
+ * int32 [batch, prompt_len+gen_len] (no shadow block; block_len and the
+ * thresholds are not used), then for every response position j the entropy
+ * of its prediction, the negative log-likelihood of d_targets[b, j] (int32
+ * [batch, gen_len], ids in [0, vocab)) and its greedy prediction, fused into
+ * the LM head (no logits in memory).  d_out: wino_row_loss [batch, gen_len].
+ * Asynchronous on `stream`. */
+wino_status wino_row_losses(wino_ctx* ctx, const wino_params* p, const int32_t* d_tokens,
+                            const int32_t* d_targets, wino_row_loss* d_out, void* stream);
+
 /* Standalone decision from given bf16 logits (the fused step's epilogue on
  * materialised logits).  d_logits: bf16 [batch, 2*block_len, vocab]; rows
  * 0..block_len-1 are Y_cur, rows block_len..2*block_len-1 Y_shad.

@@ -69,6 +69,13 @@ class wino_row_stats(C.Structure):
 
 ROW_STATS_BYTES = C.sizeof(wino_row_stats)
 
+
+class wino_row_loss(C.Structure):
+    _fields_ = [("entropy", C.c_float), ("nll", C.c_float), ("conf", C.c_float), ("argmax", C.c_int32)]
+
+
+ROW_LOSS_BYTES = C.sizeof(wino_row_loss)
+
 _vp, _i32, _u32, _sz = C.c_void_p, C.c_int32, C.c_uint32, C.c_size_t
 _P = C.POINTER
 _protos = {
@@ -80,6 +87,7 @@ _protos = {
     "wino_decode": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _P(_i32), _P(_i32), _vp]),
     "wino_epilogue_workspace_bytes": (_sz, [_i32, _i32, _i32]),
     "wino_epilogue": (_i32, [_P(wino_params), _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "wino_row_losses": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _vp]),
     "wino_debug_logits": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _vp]),
     "wino_debug_forward": (_i32, [_vp, _P(wino_params), _vp, _vp, _i32, _vp, _vp]),
     "wino_debug_gemm": (_i32, [_vp, _vp, _i32, _i32, _i32, _vp, _vp]),
@@ -189,6 +197,16 @@ def wino_decode(ctx, p: wino_params, tokens, block_start, final_step=None, strea
                            _ptr(block_start, torch.int32, "block_start"), fs, steps, C.byref(fw),
                            _stream(stream)), "wino_decode", ctx)
     return list(steps), fw.value
+
+
+def wino_row_losses(ctx, p: wino_params, tokens, targets, out, stream=None) -> None:
+    """WINO+ per-row quantities of training states (Sec. 4.3).  tokens int32
+    [B, P+G], targets int32 [B, G], out: device buffer of B*G wino_row_loss
+    (16 bytes each: entropy, nll, conf float32; argmax int32)."""
+    import torch
+    _check(lib.wino_row_losses(ctx, C.byref(p), _ptr(tokens, torch.int32, "tokens"),
+                               _ptr(targets, torch.int32, "targets"), _ptr(out, None, "out"),
+                               _stream(stream)), "wino_row_losses", ctx)
 
 
 def wino_epilogue_workspace_bytes(batch: int, block_len: int, vocab: int) -> int:

@@ -299,6 +299,55 @@ __global__ __launch_bounds__(256) void epi_stats_kernel(const uint16_t* __restri
 
 }  // namespace
 
+// WINO+ per-row quantities: one wave per row merges the n_part tile partials
+// (max, sum-exp, entropy term, best non-mask id, target logit).
+__global__ __launch_bounds__(256) void loss_merge_kernel(const LmStatsOut lm, int R,
+                                                         float4* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= R) return;
+  float m = kNegBig, s = 0.f, z = 0.f, bz = kNegBig, tz = kNegBig;
+  int bi = INT_MAX;
+  for (int j = lane; j < lm.n_part; j += 64) {
+    const size_t o = (size_t)r * lm.n_part + j;
+    const float pm = lm.pm[o], ps = lm.ps[o], pz = lm.pz[o];
+    const float mn = fmaxf(m, pm);
+    const float fa = __expf(m - mn), fb = __expf(pm - mn);
+    // sum e^{z-mn}(z-mn) over both parts, each rebased from its own max
+    z = fa * (z + (m - mn) * s) + fb * (pz + (pm - mn) * ps);
+    s = s * fa + ps * fb;
+    m = mn;
+    const float ob = lm.pb[o];
+    const int oi = lm.pi[o];
+    if (ob > bz || (ob == bz && oi < bi)) { bz = ob; bi = oi; }
+    tz = fmaxf(tz, lm.pt[o]);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const float om = __shfl_xor(m, off, 64), os = __shfl_xor(s, off, 64), oz = __shfl_xor(z, off, 64);
+    const float mn = fmaxf(m, om);
+    const float fa = __expf(m - mn), fb = __expf(om - mn);
+    z = fa * (z + (m - mn) * s) + fb * (oz + (om - mn) * os);
+    s = s * fa + os * fb;
+    m = mn;
+    const float ob = __shfl_xor(bz, off, 64);
+    const int oi = __shfl_xor(bi, off, 64);
+    if (ob > bz || (ob == bz && oi < bi)) { bz = ob; bi = oi; }
+    tz = fmaxf(tz, __shfl_xor(tz, off, 64));
+  }
+  if (lane == 0) {
+    const float ls = __logf(s);
+    // H = log S - sum e^{z-m}(z-m) / S;  -log p(t) = m + log S - z_t
+    out[r] = make_float4(ls - z / s, m + ls - tz, __expf(bz - m) / s, __int_as_float(bi));
+  }
+}
+
+hipError_t launch_loss_merge(const LmStatsOut& lm, int R, void* out, hipStream_t st) {
+  if (R <= 0) return hipSuccess;
+  loss_merge_kernel<<<(R + 3) / 4, 256, 0, st>>>(lm, R, static_cast<float4*>(out));
+  return hipGetLastError();
+}
+
 hipError_t launch_probe_verify(const StepGeom& g, const int32_t* tokens, int32_t* next_verify,
                                hipStream_t st) {
   probe_verify_kernel<<<g.B, 64, 0, st>>>(g, tokens, next_verify);

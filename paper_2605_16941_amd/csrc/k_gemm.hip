@@ -247,6 +247,7 @@ __device__ __forceinline__ void epi_lmstats(const GemmCall& c, f32x16 (&acc)[FM]
   float* red_b = red_s + WN * BM;
   float* red_t = red_b + WN * BM;
   int* red_i = reinterpret_cast<int*>(red_t + WN * BM);
+  float* red_z = reinterpret_cast<float*>(red_i + WN * BM);  // entropy term (pz only)
   float bias[FN];
 #pragma unroll
   for (int fn = 0; fn < FN; ++fn) bias[fn] = lm.bias ? lm.bias[colb + fn * 32 + (lane & 31)] : 0.f;
@@ -276,17 +277,35 @@ __device__ __forceinline__ void epi_lmstats(const GemmCall& c, f32x16 (&acc)[FM]
         const int oi = __shfl_xor(bi, o, 64);
         if (ob > bz || (ob == bz && oi < bi)) { bz = ob; bi = oi; }
       }
-      float se = 0.f;
+      float se = 0.f, sz = 0.f;
+      if (lm.pz) {
+        // sum exp(z - m) * (z - m): the entropy's expectation term, relative
+        // to the tile max so nothing cancels against a large m
 #pragma unroll
-      for (int fn = 0; fn < FN; ++fn) se += __expf(acc[fm][fn][i] + bias[fn] - mx);
+        for (int fn = 0; fn < FN; ++fn) {
+          const float u = acc[fm][fn][i] + bias[fn] - mx;
+          const float e = __expf(u);
+          se += e;
+          sz += e * u;
+        }
 #pragma unroll
-      for (int o = 16; o > 0; o >>= 1) se += __shfl_xor(se, o, 64);
+        for (int o = 16; o > 0; o >>= 1) {
+          se += __shfl_xor(se, o, 64);
+          sz += __shfl_xor(sz, o, 64);
+        }
+      } else {
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) se += __expf(acc[fm][fn][i] + bias[fn] - mx);
+#pragma unroll
+        for (int o = 16; o > 0; o >>= 1) se += __shfl_xor(se, o, 64);
+      }
       if ((lane & 31) == 0) {
         red_m[wn * BM + lrow] = mx;
         red_s[wn * BM + lrow] = se;
         red_b[wn * BM + lrow] = bz;
         red_t[wn * BM + lrow] = tz;
         red_i[wn * BM + lrow] = bi;
+        if (lm.pz) red_z[wn * BM + lrow] = sz;
       }
     }
   __syncthreads();
@@ -296,17 +315,21 @@ __device__ __forceinline__ void epi_lmstats(const GemmCall& c, f32x16 (&acc)[FM]
     float m = kNegBig;
 #pragma unroll
     for (int w = 0; w < WN; ++w) m = fmaxf(m, red_m[w * BM + r]);
-    float s = 0.f, bz = kNegBig, tz = kNegBig;
+    float s = 0.f, z = 0.f, bz = kNegBig, tz = kNegBig;
     int bi = INT_MAX;
 #pragma unroll
     for (int w = 0; w < WN; ++w) {
-      s += red_s[w * BM + r] * __expf(red_m[w * BM + r] - m);
+      const float dm = red_m[w * BM + r] - m, f = __expf(dm);
+      s += red_s[w * BM + r] * f;
+      // sum e^{z-m}(z-m) = e^{m_w-m} (sum e^{z-m_w}(z-m_w) + (m_w-m) sum e^{z-m_w})
+      if (lm.pz) z += f * (red_z[w * BM + r] + dm * red_s[w * BM + r]);
       const float ob = red_b[w * BM + r];
       const int oi = red_i[w * BM + r];
       if (ob > bz || (ob == bz && oi < bi)) { bz = ob; bi = oi; }
       tz = fmaxf(tz, red_t[w * BM + r]);
     }
     const size_t o = (size_t)row * lm.n_part + tn;
+    if (lm.pz) lm.pz[o] = z;
     lm.pm[o] = m;
     lm.ps[o] = s;
     lm.pb[o] = bz;

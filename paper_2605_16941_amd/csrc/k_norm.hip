@@ -260,15 +260,20 @@ __global__ __launch_bounds__(256) void select_norm_kernel(StepGeom g, int mode,
                                                           const uint16_t* __restrict__ gain,
                                                           float eps, int d, uint16_t* __restrict__ hf,
                                                           uint16_t* __restrict__ hf_lo,
-                                                          int32_t* __restrict__ target) {
+                                                          int32_t* __restrict__ target, int r0,
+                                                          int n, const int32_t* __restrict__ tgt_in) {
   const int lane = threadIdx.x & 63;
-  const int rows_per_seq = mode == 0 ? g.Lb : 2 * g.Lb;
+  const int rows_per_seq = mode == 0 ? g.Lb : mode == 1 ? 2 * g.Lb : g.G;
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= g.B * rows_per_seq) return;
-  const int b = r / rows_per_seq, j = r - b * rows_per_seq;
-  const int c0 = cur_start(g, b);
+  if (r >= n) return;
+  const int ra = r0 + r;  // row of the flattened [B, rows_per_seq] selection
+  const int b = ra / rows_per_seq, j = ra - b * rows_per_seq;
   int src;
-  if (mode == 0) {
+  if (mode == 2) {  // response row j (WINO+ training state, no shadow block)
+    src = g.P + j;
+    if (lane == 0) target[r] = tgt_in[ra];
+  } else if (mode == 0) {
+    const int c0 = cur_start(g, b);
     const int tok = tokens[(size_t)b * g.S + c0 + j];
     // Eq. 4: draft reads Y_cur, verify reads Y_shad (without shadow rows no
     // position is verified; the current row's statistics then go unused)
@@ -276,7 +281,7 @@ __global__ __launch_bounds__(256) void select_norm_kernel(StepGeom g, int mode,
     src = verify ? g.S + j : c0 + j;
     if (lane == 0) target[r] = verify ? tok : -1;
   } else {
-    src = j < g.Lb ? c0 + j : g.S + (j - g.Lb);
+    src = j < g.Lb ? cur_start(g, b) + j : g.S + (j - g.Lb);
     if (lane == 0) target[r] = -1;
   }
   float v[CPL][8];
@@ -325,13 +330,14 @@ void launch_residual_reduce(float* x, const float* part, int n_part, int part_ro
 
 void launch_select_norm(const StepGeom& g, int mode, const int32_t* tokens, const float* x,
                         const uint16_t* gain, float eps, int d, uint16_t* hf, uint16_t* hf_lo,
-                        int32_t* target, hipStream_t st) {
-  const int R = g.B * (mode == 0 ? g.Lb : 2 * g.Lb);
-  dim3 grid((R + 3) / 4), block(256);
-  if (d <= 512) select_norm_kernel<1><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target);
-  else if (d <= 1024) select_norm_kernel<2><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target);
-  else if (d <= 2048) select_norm_kernel<4><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target);
-  else select_norm_kernel<8><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target);
+                        int32_t* target, hipStream_t st, int r0, int n, const int32_t* tgt_in) {
+  if (mode != 2) { r0 = 0; n = g.B * (mode == 0 ? g.Lb : 2 * g.Lb); }
+  if (n <= 0) return;
+  dim3 grid((n + 3) / 4), block(256);
+  if (d <= 512) select_norm_kernel<1><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in);
+  else if (d <= 1024) select_norm_kernel<2><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in);
+  else if (d <= 2048) select_norm_kernel<4><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in);
+  else select_norm_kernel<8><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in);
 }
 
 }  // namespace wino

@@ -50,10 +50,13 @@ void launch_residual_reduce(float* x, const float* part, int n_part, int part_ro
 // Rows the decision reads.  mode 0: one row per block position (current row
 // if the token is the mask, else the shadow row) and target = current token
 // (-1 for masked).  mode 1: all 2*Lb rows (current then shadow) per sequence.
+// mode 2: response rows r0 .. r0+n-1 of the flattened [B, G] response (row
+// P + j of sequence b for r = b*G + j), target = tgt_in[r].
 // The normed row is written as hi = bf16(y) and lo = bf16(y - hi).
 void launch_select_norm(const StepGeom& g, int mode, const int32_t* tokens, const float* x,
                         const uint16_t* gain, float eps, int d, uint16_t* hf, uint16_t* hf_lo,
-                        int32_t* target, hipStream_t st);
+                        int32_t* target, hipStream_t st, int r0 = 0, int n = 0,
+                        const int32_t* tgt_in = nullptr);
 
 // --------------------------------------------------------------- GEMM
 // C = A * W^T with A bf16 [M, K] (row stride lda), W bf16 [N, K] (row stride
@@ -76,6 +79,7 @@ struct LmStatsOut {   // LM head + streaming softmax statistics per (row, N-tile
   float* pb;          // [M, n_part] max logit over ids != mask
   int32_t* pi;        // [M, n_part] lowest id reaching pb
   float* pt;          // [M, n_part] logit of target (kNegBig if not in tile)
+  float* pz;          // [M, n_part] sum exp(z - pm) * (z - pm) (entropy), or null
 };
 
 enum GemmEpi {
@@ -162,6 +166,10 @@ struct DecideArgs {
   int32_t* next_verify;
 };
 hipError_t launch_decide(const DecideArgs& a, hipStream_t st);
+// WINO+ per-row quantities (Sec. 4.3) from LM-head partials of R rows (pz
+// required): out[r] = {entropy, nll of the target, greedy confidence, argmax}
+// (wino_loss_row layout).
+hipError_t launch_loss_merge(const LmStatsOut& lm, int R, void* out, hipStream_t st);
 // next_verify[b] as above for the state before any step (fused-step layout).
 hipError_t launch_probe_verify(const StepGeom& g, const int32_t* tokens, int32_t* next_verify,
                                hipStream_t st);

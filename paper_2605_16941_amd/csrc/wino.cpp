@@ -31,7 +31,9 @@ constexpr int kMaxSplits = 8;
 int round64(int v) { return (v + 63) / 64 * 64; }
 
 struct Layout {
-  size_t x, h, q, k, vt, att, u, hf, hf_lo, part, target, rope_cos, rope_sin, pm, ps, pb, pi, pt, misc, total;
+  size_t x, h, q, k, vt, att, u, hf, hf_lo, part, target, rope_cos, rope_sin, pm, ps, pb, pi, pt, pz, misc,
+      total;
+  size_t rows;  // rows the LM-head partials hold
   int max_part;
   size_t part_elems;  // split-K partial buffer (fp32 elements)
 };
@@ -65,6 +67,8 @@ Layout make_layout(const wino_model_config& c, int max_batch, int max_seq) {
   L.pb = take(P * 4);
   L.pi = take(P * 4);
   L.pt = take(P * 4);
+  L.pz = take(P * 4);
+  L.rows = R;
   L.misc = take((size_t)max_batch * 4 * 4);
   L.total = off;
   return L;
@@ -561,6 +565,56 @@ wino_status wino_decode(wino_ctx* c, const wino_params* p, int32_t* d_tokens, in
   if (h_steps_per_seq)
     HIP_TRY(c, hipMemcpy(h_steps_per_seq, c->seq_steps(), sizeof(int32_t) * B, hipMemcpyDeviceToHost));
   if (h_forward_passes) *h_forward_passes = forwards;
+  return WINO_OK;
+}
+
+wino_status wino_row_losses(wino_ctx* c, const wino_params* p, const int32_t* d_tokens,
+                            const int32_t* d_targets, wino_row_loss* d_out, void* stream) {
+  if (!c) return WINO_ERR_INVALID_ARG;
+  wino_status s = validate_params(c, p);
+  if (s != WINO_OK) return s;
+  if (!d_tokens || !d_targets || !d_out) return WINO_ERR_INVALID_ARG;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const wino_model_config& m = c->cfg;
+  // a plain forward: no shadow rows, so the block cursor is never read for
+  // positions (any valid [B] int32 buffer serves as its pointer)
+  const StepGeom g = make_geom(p, c->block_steps(), false);
+  s = run_forward(c, g, d_tokens, 2 * m.n_layers, st);
+  if (s != WINO_OK) return s;
+  GemmCall lc{};
+  lc.A = c->hf(); lc.A2 = c->hf_lo(); lc.lda = m.d_model; lc.W = c->lm_head; lc.ldw = m.d_model;
+  lc.N = m.vocab; lc.K = m.d_model; lc.epi = EPI_LMSTATS;
+  const long total = (long)g.B * g.G;
+  const int chunk = (int)std::min<size_t>(c->L.rows, 1 << 20);
+  for (long r0 = 0; r0 < total; r0 += chunk) {
+    const int n = (int)std::min<long>(chunk, total - r0);
+    {
+      Bracket br(c, K_SELECT_NORM, st);
+      launch_select_norm(g, 2, d_tokens, c->x(), c->final_norm, m.rms_eps, m.d_model, c->hf(), c->hf_lo(),
+                         c->target(), st, (int)r0, n, d_targets);
+      HIP_TRY(c, hipGetLastError());
+      br.done(0, (double)n * m.d_model * 8);
+    }
+    lc.M = n;
+    const int bn = gemm_tile_n(lc);
+    if (bn == 0) { c->err = "no LM-head tile for this shape"; return WINO_ERR_UNSUPPORTED; }
+    const int n_part = m.vocab / bn;
+    if (n_part > c->L.max_part) { c->err = "LM-head partials exceed the workspace"; return WINO_ERR_UNSUPPORTED; }
+    lc.lm = LmStatsOut{c->lm_bias, c->target(), p->mask_id, n_part, c->at<float>(c->L.pm),
+                       c->at<float>(c->L.ps), c->at<float>(c->L.pb), c->at<int32_t>(c->L.pi),
+                       c->at<float>(c->L.pt), c->at<float>(c->L.pz)};
+    {
+      Bracket br(c, K_LM_HEAD, st);
+      HIP_TRY(c, launch_gemm(lc, st));
+      br.done(2.0 * n * (double)m.vocab * m.d_model,
+              2.0 * ((double)n * m.d_model + (double)m.vocab * m.d_model) + 24.0 * n * n_part);
+    }
+    {
+      Bracket br(c, K_DECIDE, st);
+      HIP_TRY(c, launch_loss_merge(lc.lm, n, d_out + r0, st));
+      br.done(0, 24.0 * n * n_part + 16.0 * n);
+    }
+  }
   return WINO_OK;
 }
 

@@ -38,6 +38,7 @@ def test_struct_sizes_match_header_layout(abi):
     assert C.sizeof(abi.wino_model_config) == 32
     assert C.sizeof(abi.wino_params) == 40
     assert C.sizeof(abi.wino_row_stats) == 24
+    assert C.sizeof(abi.wino_row_loss) == 16
     assert C.sizeof(abi.wino_weights) == 10 * C.sizeof(C.c_void_p)
 
 

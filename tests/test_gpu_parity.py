@@ -465,6 +465,48 @@ def test_baseline_decoders_match_oracle(P, m):
     model.close()
 
 
+LOSS_DT = np.dtype([("entropy", "<f4"), ("nll", "<f4"), ("conf", "<f4"), ("argmax", "<i4")])
+
+
+@pytest.mark.parametrize("variant", ["literal", "wide"])
+def test_row_losses_match_oracle(P, variant):
+    """WINO+ per-row quantities (Sec. 4.3) of training states: entropy, target
+    NLL and greedy prediction of every response row, fused into the LM head.
+    Two sequences whose training states reveal the tokens finalized before
+    different steps; 128 response rows in chunks of the workspace's rows."""
+    from oracle import losses as LS
+    cfg, w = tiny(variant, seed=3)
+    wd = to_device(w)
+    p, g, lb, B = 32, 64, 16, 2
+    model = P.WinoModel(cfg, wd, B, p + g + lb)
+    prm_c = P.make_params(B, p, g, lb, cfg.mask_id)
+    rng = np.random.default_rng(5)
+    final = batch_tokens(cfg, B, p, g, seed=6, fill=[(0, g, 1.0)])
+    t_fin = np.concatenate([np.zeros((B, p), int), rng.integers(1, 9, (B, g))], axis=1)
+    states = np.stack([LS.training_state(final[b], t_fin[b], t, p, cfg.mask_id)
+                       for b, t in enumerate([3, 6])])
+    targets = final[:, p:]
+    out = torch.zeros(B * g * LOSS_DT.itemsize, dtype=torch.uint8, device="cuda")
+    P.wino_row_losses(model.ctx, prm_c, torch.tensor(states, dtype=torch.int32, device="cuda"),
+                      torch.tensor(targets, dtype=torch.int32, device="cuda"), out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().view(LOSS_DT).reshape(B, g)
+    for b in range(B):
+        for act_round, tol in ((M.round_bf16, 5e-3), (None, 2e-2)):
+            z = LS.state_logits(w, cfg, states[b], p, act_round)
+            e, nll, conf, yhat = LS.row_quantities(z, targets[b], cfg.mask_id)
+            assert np.max(np.abs(got[b]["entropy"] - e)) < 2 * tol
+            assert np.max(np.abs(got[b]["nll"] - nll) / (1 + nll)) < 2 * tol
+            assert np.max(np.abs(got[b]["conf"] - conf)) < tol
+            if act_round is not None:
+                pr = W.softmax_rows(z)
+                pr[:, cfg.mask_id] = -1.0
+                top = np.sort(pr, axis=-1)
+                sure = top[:, -1] - top[:, -2] > 1e-2
+                assert sure.any() and np.array_equal(got[b]["argmax"][sure], yhat[sure])
+    model.close()
+
+
 def test_step_is_deterministic(P):
     cfg, w = tiny("wide", seed=6)
     wd = to_device(w)
