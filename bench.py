@@ -128,14 +128,17 @@ def run_workload(P, wi, cfg, weights, name, steps, warmup, profile_dominant=True
 
 def run_baselines(P, wi, cfg, weights, name, ms=(1, 4)):
     """Full decodes from the prompt with the Sec. 3 baselines (tokens_per_step
-    m: 1 = Eq. 1 greedy, m > 1 naive parallel sampling) on the same kernels,
-    next to WINO: forwards, tokens/s and WINO's step reduction / speedup."""
+    m: 1 = Eq. 1 greedy, m > 1 naive parallel sampling) and the single-threshold
+    rule of WINO+ inference (tau2 = 0: draft only, no shadow block) on the same
+    kernels, next to WINO: forwards, tokens/s and WINO's step reduction /
+    speedup.  Synthetic weights: the ratios show the mechanism, not accuracy."""
     import torch
     preset, B, p, g, lb, tau1, tau2, img = CONFIGS[name]
     model = P.WinoModel(cfg, weights, B, p + g + lb)
     out = {}
-    for label, m in [("wino", 0)] + [(f"tokens_per_step_{m}", m) for m in ms]:
-        prm = P.make_params(B, p, g, lb, cfg.mask_id, tau1, tau2, tokens_per_step=m)
+    runs = [("wino", 0, tau2), ("single_threshold", 0, 0.0)] + [(f"tokens_per_step_{m}", m, tau2) for m in ms]
+    for label, m, t2 in runs:
+        prm = P.make_params(B, p, g, lb, cfg.mask_id, tau1, t2, tokens_per_step=m)
         tok = wi.initial_tokens(wi.prompts(cfg, B, p, seed=1000, image_prefix=img), g, cfg.mask_id).cuda()
         bs = torch.zeros(B, dtype=torch.int32, device="cuda")
         torch.cuda.synchronize()

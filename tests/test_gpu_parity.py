@@ -288,7 +288,8 @@ def test_teacher_forced_steps(P, variant, tau1, tau2):
 
 # ---------------------------------------------------------------- free-running decode
 @pytest.mark.parametrize("variant,tau1,tau2,lb", [("wide", 0.7, 0.9, 16), ("literal", 0.7, 0.9, 16),
-                                                  ("wide", 0.6, 0.9, 64), ("wide", 0.8, 0.95, 8)])
+                                                  ("wide", 0.6, 0.9, 64), ("wide", 0.8, 0.95, 8),
+                                                  ("wide", 0.9, 0.0, 16)])
 def test_decode_matches_oracle(P, variant, tau1, tau2, lb):
     cfg, w = tiny(variant, seed=2)
     wd = to_device(w)
