@@ -587,7 +587,7 @@ constexpr TileCfg kTiles[] = {
     {128, 256, 2, 2, 64, 2, 1, 0.76f},  // 2
     {128, 128, 2, 2, 64, 2, 2, 0.78f},  // 3
     {64, 128, 2, 2, 64, 2, 3, 0.64f},   // 4
-    {32, 256, 1, 4, 64, 2, 2, 0.95f},   // 5
+    {32, 256, 1, 4, 64, 2, 2, 0.60f},   // 5
     {256, 256, 4, 2, 64, 2, 1, 1.00f},  // 6  (8 waves)
     {256, 256, 2, 4, 64, 2, 1, 0.98f},  // 7  (8 waves)
     {128, 256, 2, 4, 64, 2, 1, 0.74f},  // 8  (8 waves)
