@@ -83,7 +83,7 @@ def run_workload(P, wi, cfg, weights, name, steps, warmup, profile_dominant=True
     for _ in range(warmup):
         one_step()
     torch.cuda.synchronize()
-    classes = {P.wino_kernel_class_name(i): i for i in range(12)}
+    classes = {P.wino_kernel_class_name(i): i for i in range(P._abi.N_KERNEL_CLASSES)}
     if profile_dominant:
         P.wino_profile(model.ctx, 1 << classes[DOMINANT])
     torch.cuda.synchronize()
@@ -96,7 +96,7 @@ def run_workload(P, wi, cfg, weights, name, steps, warmup, profile_dominant=True
     P.wino_profile(model.ctx, 0)
 
     # per-kernel breakdown (separate pass, not part of the timed value)
-    P.wino_profile(model.ctx, (1 << 12) - 1)
+    P.wino_profile(model.ctx, (1 << P._abi.N_KERNEL_CLASSES) - 1)
     for _ in range(2):
         one_step()
     torch.cuda.synchronize()

@@ -232,7 +232,7 @@ wino_status wino_debug_gemm(const void* d_A, const void* d_W, int32_t M, int32_t
  * synchronises, then reports per class: launches, total milliseconds and the
  * algorithmic flops and HBM bytes those launches represent; it resets the
  * counters.  Arrays have WINO_N_KERNEL_CLASSES entries. */
-#define WINO_N_KERNEL_CLASSES 12
+#define WINO_N_KERNEL_CLASSES 13
 wino_status wino_profile(wino_ctx* ctx, uint32_t class_mask);
 wino_status wino_profile_read(wino_ctx* ctx, int64_t* h_launches, double* h_ms,
                               double* h_flops, double* h_bytes);

@@ -33,7 +33,7 @@ def _load():
 
 lib = _load()
 
-N_KERNEL_CLASSES = 12
+N_KERNEL_CLASSES = 13
 WINO_FLAG_NO_FORCE_TOP1 = 0x1
 WINO_FLAG_NO_CAP_FILL = 0x2
 KEEP, DRAFT, REMASK, FORCED, CAPFILL = 0, 1, 2, 3, 4

@@ -38,7 +38,10 @@ __device__ __forceinline__ int perm_key(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
-template <int HD, int NW>
+// CQ (compact queries): only each sequence's current-block rows and shadow
+// rows are queried - compact query i < Lb is row c0 + i, i >= Lb is row
+// S + i - Lb - and output row i of sequence b goes to o row b*(Lb+Ls) + i.
+template <int HD, int NW, bool CQ>
 __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const uint16_t* __restrict__ q,
                                                        const uint16_t* __restrict__ k,
                                                        const uint16_t* __restrict__ vt, int H,
@@ -57,8 +60,11 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
   const int b = blockIdx.z, h = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, grp = lane >> 5;
   const int q0 = blockIdx.x * (NW * 32);
-  const int myq = q0 + wave * 32 + (lane & 31);
   const int c0 = cur_start(g, b);
+  const int NQ = g.Lb + g.Ls;                    // compact queries per sequence
+  const int ci = q0 + wave * 32 + (lane & 31);   // compact query index (CQ)
+  const bool qvalid = CQ ? ci < NQ : q0 + wave * 32 + (lane & 31) < g.T;
+  const int myq = CQ ? (ci < g.Lb ? c0 + ci : g.S + (ci - g.Lb)) : q0 + wave * 32 + (lane & 31);
   const bool shadow = myq >= g.S;
   const int excl = shadow ? c0 + (myq - g.S) : -1;
   const int klim = shadow ? g.T : g.S;
@@ -107,7 +113,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
 
   bf16x8 qf[KS];
   {
-    const int qrow = myq < g.T ? myq : g.T - 1;
+    const int qrow = qvalid && myq < g.T ? myq : g.T - 1;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
       qf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qb + (size_t)qrow * HD + ks * 16 + grp * 8));
@@ -120,8 +126,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
     for (int i = 0; i < 16; ++i) oacc[fe][i] = 0.f;
   float mrun = kNegBig, lrun = 0.f;
 
-  const int q_last = min(q0 + NW * 32, g.T) - 1;
-  const bool has_shadow = q_last >= g.S;
+  const bool has_shadow = CQ ? g.Ls > 0 && q0 + NW * 32 > g.Lb : min(q0 + NW * 32, g.T) - 1 >= g.S;
   const int kend = has_shadow ? g.T : g.S;  // shadow rows also see keys S..T-1
   const int ntile = (kend + BKV - 1) / BKV;
 
@@ -232,9 +237,10 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
   }
 
   lrun += __shfl_xor(lrun, 32, 64);
-  if (myq < g.T) {
+  if (qvalid) {
     const float inv = 1.f / lrun;
-    uint16_t* dst = o + ((size_t)b * g.T + myq) * (size_t)(H * HD) + (size_t)h * HD;
+    const size_t orow = CQ ? (size_t)b * NQ + ci : (size_t)b * g.T + myq;
+    uint16_t* dst = o + orow * (size_t)(H * HD) + (size_t)h * HD;
 #pragma unroll
     for (int fe = 0; fe < FE; ++fe)
 #pragma unroll
@@ -250,16 +256,21 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
 
 template <int HD>
 hipError_t launch_hd(const StepGeom& g, const uint16_t* q, const uint16_t* k, const uint16_t* vt,
-                     int H, uint16_t* o, float scale_log2, hipStream_t st) {
+                     int H, uint16_t* o, float scale_log2, bool compact, hipStream_t st) {
+  if (compact) {
+    dim3 grid((g.Lb + g.Ls + 63) / 64, H, g.B);
+    attn_kernel<HD, 2, true><<<grid, 128, 0, st>>>(g, q, k, vt, H, o, scale_log2);
+    return hipGetLastError();
+  }
   // 128-query workgroups when there are enough of them to fill the chip,
   // otherwise 64-query ones (more workgroups per head).
   const long wg128 = (long)((g.T + 127) / 128) * H * g.B;
   if (wg128 >= 512) {
     dim3 grid((g.T + 127) / 128, H, g.B);
-    attn_kernel<HD, 4><<<grid, 256, 0, st>>>(g, q, k, vt, H, o, scale_log2);
+    attn_kernel<HD, 4, false><<<grid, 256, 0, st>>>(g, q, k, vt, H, o, scale_log2);
   } else {
     dim3 grid((g.T + 63) / 64, H, g.B);
-    attn_kernel<HD, 2><<<grid, 128, 0, st>>>(g, q, k, vt, H, o, scale_log2);
+    attn_kernel<HD, 2, false><<<grid, 128, 0, st>>>(g, q, k, vt, H, o, scale_log2);
   }
   return hipGetLastError();
 }
@@ -267,10 +278,11 @@ hipError_t launch_hd(const StepGeom& g, const uint16_t* q, const uint16_t* k, co
 }  // namespace
 
 hipError_t launch_attention(const StepGeom& g, const uint16_t* q, const uint16_t* k,
-                            const uint16_t* vt, int H, int hd, uint16_t* o, hipStream_t st) {
+                            const uint16_t* vt, int H, int hd, uint16_t* o, hipStream_t st,
+                            bool compact) {
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
-  if (hd == 128) return launch_hd<128>(g, q, k, vt, H, o, scale_log2, st);
-  if (hd == 64) return launch_hd<64>(g, q, k, vt, H, o, scale_log2, st);
+  if (hd == 128) return launch_hd<128>(g, q, k, vt, H, o, scale_log2, compact, st);
+  if (hd == 64) return launch_hd<64>(g, q, k, vt, H, o, scale_log2, compact, st);
   return hipErrorInvalidValue;
 }
 

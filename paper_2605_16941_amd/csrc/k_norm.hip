@@ -261,7 +261,8 @@ __global__ __launch_bounds__(256) void select_norm_kernel(StepGeom g, int mode,
                                                           float eps, int d, uint16_t* __restrict__ hf,
                                                           uint16_t* __restrict__ hf_lo,
                                                           int32_t* __restrict__ target, int r0,
-                                                          int n, const int32_t* __restrict__ tgt_in) {
+                                                          int n, const int32_t* __restrict__ tgt_in,
+                                                          int compact) {
   const int lane = threadIdx.x & 63;
   const int rows_per_seq = mode == 0 ? g.Lb : mode == 1 ? 2 * g.Lb : g.G;
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -279,14 +280,28 @@ __global__ __launch_bounds__(256) void select_norm_kernel(StepGeom g, int mode,
     // position is verified; the current row's statistics then go unused)
     const bool verify = tok != g.mask_id && g.Ls > 0;
     src = verify ? g.S + j : c0 + j;
+    if (compact) src = verify ? g.Lb + j : j;  // gathered rows: current block, then shadow
     if (lane == 0) target[r] = verify ? tok : -1;
   } else {
     src = j < g.Lb ? cur_start(g, b) + j : g.S + (j - g.Lb);
     if (lane == 0) target[r] = -1;
   }
   float v[CPL][8];
-  const float ss = load_row_f32<CPL>(x + ((size_t)b * g.T + src) * d, d, lane, v);
+  const size_t xrow = compact ? (size_t)b * (g.Lb + g.Ls) + src : (size_t)b * g.T + src;
+  const float ss = load_row_f32<CPL>(x + xrow * d, d, lane, v);
   norm_store<CPL>(v, ss, gain, eps, d, lane, hf + (size_t)r * d, hf_lo + (size_t)r * d);
+}
+
+// Copy of the current-block and shadow rows of every sequence (fp32).
+__global__ __launch_bounds__(256) void gather_block_rows_kernel(StepGeom g, const float* __restrict__ x,
+                                                                int d, float* __restrict__ xc) {
+  const int nq = g.Lb + g.Ls;
+  const int r = blockIdx.x;  // b * nq + i
+  const int b = r / nq, i = r - b * nq;
+  const int t = i < g.Lb ? cur_start(g, b) + i : g.S + (i - g.Lb);
+  const float4* src = reinterpret_cast<const float4*>(x + ((size_t)b * g.T + t) * d);
+  float4* dst = reinterpret_cast<float4*>(xc + (size_t)r * d);
+  for (int c = threadIdx.x; c < d / 4; c += 256) dst[c] = src[c];
 }
 
 }  // namespace
@@ -330,14 +345,22 @@ void launch_residual_reduce(float* x, const float* part, int n_part, int part_ro
 
 void launch_select_norm(const StepGeom& g, int mode, const int32_t* tokens, const float* x,
                         const uint16_t* gain, float eps, int d, uint16_t* hf, uint16_t* hf_lo,
-                        int32_t* target, hipStream_t st, int r0, int n, const int32_t* tgt_in) {
+                        int32_t* target, hipStream_t st, int r0, int n, const int32_t* tgt_in,
+                        bool compact) {
   if (mode != 2) { r0 = 0; n = g.B * (mode == 0 ? g.Lb : 2 * g.Lb); }
+  if (mode != 0) compact = false;
   if (n <= 0) return;
   dim3 grid((n + 3) / 4), block(256);
-  if (d <= 512) select_norm_kernel<1><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in);
-  else if (d <= 1024) select_norm_kernel<2><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in);
-  else if (d <= 2048) select_norm_kernel<4><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in);
-  else select_norm_kernel<8><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in);
+  const int cp = compact ? 1 : 0;
+  if (d <= 512) select_norm_kernel<1><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in, cp);
+  else if (d <= 1024) select_norm_kernel<2><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in, cp);
+  else if (d <= 2048) select_norm_kernel<4><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in, cp);
+  else select_norm_kernel<8><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in, cp);
+}
+
+void launch_gather_block_rows(const StepGeom& g, const float* x, int d, float* xc, hipStream_t st) {
+  const int rows = g.B * (g.Lb + g.Ls);
+  if (rows > 0) gather_block_rows_kernel<<<rows, 256, 0, st>>>(g, x, d, xc);
 }
 
 }  // namespace wino

@@ -47,16 +47,21 @@ void launch_rmsnorm(float* x, const uint16_t* gain, float eps, int M, int d, uin
 // part_row0 <= m < M.
 void launch_residual_reduce(float* x, const float* part, int n_part, int part_row0, int M, int d,
                             hipStream_t st);
+// xc[b*(Lb+Ls) + i] = x row c0+i (i < Lb) or S+i-Lb (the shadow rows): the
+// rows of the current block and the shadow block, fp32 [B*(Lb+Ls), d].
+void launch_gather_block_rows(const StepGeom& g, const float* x, int d, float* xc, hipStream_t st);
 // Rows the decision reads.  mode 0: one row per block position (current row
 // if the token is the mask, else the shadow row) and target = current token
 // (-1 for masked).  mode 1: all 2*Lb rows (current then shadow) per sequence.
 // mode 2: response rows r0 .. r0+n-1 of the flattened [B, G] response (row
 // P + j of sequence b for r = b*G + j), target = tgt_in[r].
 // The normed row is written as hi = bf16(y) and lo = bf16(y - hi).
+// With compact (mode 0 only) x holds the gathered block rows of
+// launch_gather_block_rows instead of the full [B, T] stream.
 void launch_select_norm(const StepGeom& g, int mode, const int32_t* tokens, const float* x,
                         const uint16_t* gain, float eps, int d, uint16_t* hf, uint16_t* hf_lo,
                         int32_t* target, hipStream_t st, int r0 = 0, int n = 0,
-                        const int32_t* tgt_in = nullptr);
+                        const int32_t* tgt_in = nullptr, bool compact = false);
 
 // --------------------------------------------------------------- GEMM
 // C = A * W^T with A bf16 [M, K] (row stride lda), W bf16 [N, K] (row stride
@@ -130,8 +135,11 @@ void plan_residual_gemm(GemmCall& c, size_t part_elems);
 // Bidirectional attention with the WINO shadow mask (Sec. 4.2.2): query row
 // t < S sees keys [0, S); shadow query S+j sees keys [0, T) except c0+j.
 // o: bf16 [B*T, H*hd] row-major.
+// compact: query only each sequence's Lb current-block rows and Ls shadow
+// rows; o then holds those rows, [B * (Lb + Ls), H*hd] (current rows first).
 hipError_t launch_attention(const StepGeom& g, const uint16_t* q, const uint16_t* k,
-                            const uint16_t* vt, int H, int hd, uint16_t* o, hipStream_t st);
+                            const uint16_t* vt, int H, int hd, uint16_t* o, hipStream_t st,
+                            bool compact = false);
 
 // --------------------------------------------------------------- decision
 // Per-position decision codes (same values as the public WINO_* flags).

@@ -20,19 +20,20 @@ namespace {
 
 enum KClass {
   K_EMBED_NORM = 0, K_RMSNORM, K_GEMM_QKV, K_ATTENTION, K_GEMM_O, K_GEMM_GATEUP, K_GEMM_DOWN,
-  K_SELECT_NORM, K_LM_HEAD, K_DECIDE, K_EPI_STATS, K_GEMM_DEBUG
+  K_SELECT_NORM, K_LM_HEAD, K_DECIDE, K_EPI_STATS, K_GEMM_DEBUG, K_GEMM_LAST
 };
 const char* kClassNames[WINO_N_KERNEL_CLASSES] = {
     "embed_norm", "rmsnorm", "gemm_qkv_rope", "attention", "gemm_o_residual", "gemm_gateup_swiglu",
-    "gemm_down_residual", "select_norm", "lm_head_stats", "decide", "epilogue_stats", "gemm_logits"};
+    "gemm_down_residual", "select_norm", "lm_head_stats", "decide", "epilogue_stats", "gemm_logits",
+    "gemm_last_layer_rows"};
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 constexpr int kMaxSplits = 8;
 int round64(int v) { return (v + 63) / 64 * 64; }
 
 struct Layout {
-  size_t x, h, q, k, vt, att, u, hf, hf_lo, part, target, rope_cos, rope_sin, pm, ps, pb, pi, pt, pz, misc,
-      total;
+  size_t x, h, q, k, vt, att, u, hf, hf_lo, xc, part, target, rope_cos, rope_sin, pm, ps, pb, pi, pt, pz,
+      misc, total;
   size_t rows;  // rows the LM-head partials hold
   int max_part;
   size_t part_elems;  // split-K partial buffer (fp32 elements)
@@ -54,8 +55,9 @@ Layout make_layout(const wino_model_config& c, int max_batch, int max_seq) {
   L.vt = take((size_t)max_batch * H * Tp * hd * 2);
   L.att = take(M * d * 2);
   L.u = take(M * F * 2);
-  L.hf = take(M * d * 2);
-  L.hf_lo = take(M * d * 2);
+  L.hf = take(2 * R * d * 2);    // selected rows (hi, lo) for the LM head: up to
+  L.hf_lo = take(2 * R * d * 2); // 2 * Lb per sequence (the test entry point)
+  L.xc = take(2 * R * d * 4);    // last layer's current-block and shadow rows
   L.part_elems = (size_t)kMaxSplits * std::min<size_t>(M, 1024) * d;
   L.part = take(L.part_elems * 4);
   L.target = take(M * 4);
@@ -100,6 +102,7 @@ struct wino_ctx {
 
   template <class T> T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
   float* x() const { return at<float>(L.x); }
+  float* xc() const { return at<float>(L.xc); }
   uint16_t* h() const { return at<uint16_t>(L.h); }
   uint16_t* q() const { return at<uint16_t>(L.q); }
   uint16_t* k() const { return at<uint16_t>(L.k); }
@@ -213,12 +216,19 @@ double norm_bytes(int M, int d, const Pending& p) {
 
 // Embedding and the first n_sub sublayers (attention and FFN halves of each
 // layer, in order); leaves the residual stream in x.
+// With compact, the last layer's attention queries, O projection and FFN run
+// only on each sequence's current-block and shadow rows (the only rows the
+// decision reads; keys and values still come from every row), gathered into
+// xc = [B * (Lb + Ls), d]; the caller then reads the final rows from xc.
 wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, int n_sub,
-                        hipStream_t st) {
+                        hipStream_t st, bool compact = false) {
   const wino_model_config& m = c->cfg;
   const int d = m.d_model, F = m.d_ff, H = m.n_heads, hd = m.head_dim;
   const int M = g.B * g.T;
+  compact = compact && n_sub >= 2 * m.n_layers;
   Pending pend;  // split-K partials not yet added to x
+  float* xr = c->x();  // residual stream of the rows being computed
+  int Mr = M;
   {
     Bracket br(c, K_EMBED_NORM, st);
     launch_embed_norm(g, tokens, c->tok_emb, m.vocab, c->attn_norm[0], m.rms_eps, d, c->x(), c->h(), st);
@@ -236,47 +246,58 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
       HIP_TRY(c, launch_gemm(qc, st));
       br.done(2.0 * M * 3.0 * d * d, 2.0 * ((double)M * d + 3.0 * d * d + 3.0 * M * d));
     }
+    const bool last_compact = compact && l == m.n_layers - 1;
     {
       Bracket br(c, K_ATTENTION, st);
-      HIP_TRY(c, launch_attention(g, c->q(), c->k(), c->vt(), H, hd, c->att(), st));
-      const double pairs = (double)g.S * g.S + (double)g.Ls * (g.T - 1);
+      HIP_TRY(c, launch_attention(g, c->q(), c->k(), c->vt(), H, hd, c->att(), st, last_compact));
+      const double pairs = last_compact
+                               ? (double)g.Lb * g.S + (double)g.Ls * (g.T - 1)
+                               : (double)g.S * g.S + (double)g.Ls * (g.T - 1);
       br.done(4.0 * hd * H * g.B * pairs, 2.0 * 4.0 * M * d);
+    }
+    if (last_compact) {
+      Bracket br(c, K_RMSNORM, st);
+      launch_gather_block_rows(g, c->x(), d, c->xc(), st);
+      HIP_TRY(c, hipGetLastError());
+      xr = c->xc();
+      Mr = g.B * (g.Lb + g.Ls);
+      br.done(0, 8.0 * Mr * d);
     }
     GemmCall oc{};
     oc.A = c->att(); oc.lda = d; oc.W = c->w_o[l]; oc.ldw = d;
-    oc.M = M; oc.N = d; oc.K = d; oc.epi = EPI_RESIDUAL; oc.outf = c->x(); oc.ldc = d;
+    oc.M = Mr; oc.N = d; oc.K = d; oc.epi = EPI_RESIDUAL; oc.outf = xr; oc.ldc = d;
     {
-      Bracket br(c, K_GEMM_O, st);
+      Bracket br(c, xr == c->x() ? K_GEMM_O : K_GEMM_LAST, st);
       hipError_t e;
       pend = residual_gemm(c, oc, st, &e);
       HIP_TRY(c, e);
-      br.done(2.0 * M * d * d, 2.0 * ((double)M * d + (double)d * d) + 8.0 * M * d);
+      br.done(2.0 * Mr * d * d, 2.0 * ((double)Mr * d + (double)d * d) + 8.0 * Mr * d);
     }
     if (2 * l + 1 >= n_sub) break;
     {
       Bracket br(c, K_RMSNORM, st);
-      launch_rmsnorm(c->x(), c->ffn_norm[l], m.rms_eps, M, d, c->h(), c->part(), pend.n, pend.row0, st);
+      launch_rmsnorm(xr, c->ffn_norm[l], m.rms_eps, Mr, d, c->h(), c->part(), pend.n, pend.row0, st);
       HIP_TRY(c, hipGetLastError());
-      br.done(0, norm_bytes(M, d, pend));
+      br.done(0, norm_bytes(Mr, d, pend));
       pend = Pending{};
     }
     GemmCall gc{};
     gc.A = c->h(); gc.lda = d; gc.W = c->w_gu[l]; gc.ldw = d;
-    gc.M = M; gc.N = 2 * F; gc.K = d; gc.epi = EPI_SWIGLU; gc.outh = c->u(); gc.ldc = F; gc.F = F;
+    gc.M = Mr; gc.N = 2 * F; gc.K = d; gc.epi = EPI_SWIGLU; gc.outh = c->u(); gc.ldc = F; gc.F = F;
     {
-      Bracket br(c, K_GEMM_GATEUP, st);
+      Bracket br(c, xr == c->x() ? K_GEMM_GATEUP : K_GEMM_LAST, st);
       HIP_TRY(c, launch_gemm(gc, st));
-      br.done(2.0 * M * 2.0 * F * d, 2.0 * ((double)M * d + 2.0 * F * d + (double)M * F));
+      br.done(2.0 * Mr * 2.0 * F * d, 2.0 * ((double)Mr * d + 2.0 * F * d + (double)Mr * F));
     }
     GemmCall dc{};
     dc.A = c->u(); dc.lda = F; dc.W = c->w_down[l]; dc.ldw = F;
-    dc.M = M; dc.N = d; dc.K = F; dc.epi = EPI_RESIDUAL; dc.outf = c->x(); dc.ldc = d;
+    dc.M = Mr; dc.N = d; dc.K = F; dc.epi = EPI_RESIDUAL; dc.outf = xr; dc.ldc = d;
     {
-      Bracket br(c, K_GEMM_DOWN, st);
+      Bracket br(c, xr == c->x() ? K_GEMM_DOWN : K_GEMM_LAST, st);
       hipError_t e;
       pend = residual_gemm(c, dc, st, &e);
       HIP_TRY(c, e);
-      br.done(2.0 * M * (double)F * d, 2.0 * ((double)M * F + (double)F * d) + 8.0 * M * d);
+      br.done(2.0 * Mr * (double)F * d, 2.0 * ((double)Mr * F + (double)F * d) + 8.0 * Mr * d);
     }
     if (l + 1 < m.n_layers && 2 * (l + 1) < n_sub) {
       Bracket br(c, K_RMSNORM, st);
@@ -289,9 +310,9 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
   }
   if (pend.n) {
     Bracket br(c, K_RMSNORM, st);
-    launch_residual_reduce(c->x(), c->part(), pend.n, pend.row0, M, d, st);
+    launch_residual_reduce(xr, c->part(), pend.n, pend.row0, Mr, d, st);
     HIP_TRY(c, hipGetLastError());
-    const double rows = M - pend.row0;
+    const double rows = Mr - pend.row0;
     br.done(0, rows * d * 8 + 4.0 * rows * d * pend.n);
   }
   return WINO_OK;
@@ -308,13 +329,13 @@ wino_status step_impl(wino_ctx* c, const wino_params* p, int32_t* tokens, int32_
   const wino_model_config& m = c->cfg;
   shadow = shadow && p->tokens_per_step == 0;  // the baselines never verify
   const StepGeom g = make_geom(p, block_start, shadow);
-  wino_status s = run_forward(c, g, tokens, 2 * m.n_layers, st);
+  wino_status s = run_forward(c, g, tokens, 2 * m.n_layers, st, true);
   if (s != WINO_OK) return s;
   const int R = g.B * g.Lb;
   {
     Bracket br(c, K_SELECT_NORM, st);
-    launch_select_norm(g, 0, tokens, c->x(), c->final_norm, m.rms_eps, m.d_model, c->hf(), c->hf_lo(),
-                       c->target(), st);
+    launch_select_norm(g, 0, tokens, c->xc(), c->final_norm, m.rms_eps, m.d_model, c->hf(), c->hf_lo(),
+                       c->target(), st, 0, 0, nullptr, true);
     HIP_TRY(c, hipGetLastError());
     br.done(0, (double)R * m.d_model * 6);
   }
