@@ -103,6 +103,8 @@ def run_workload(P, wi, cfg, weights, name, steps, warmup, profile_dominant=True
     per = P.wino_profile_read(model.ctx)
     P.wino_profile(model.ctx, 0)
     kernels = {}
+    step_flops = sum(v["flops"] for v in per.values()) / 2
+    step_bytes = sum(v["bytes"] for v in per.values()) / 2
     for k, v in per.items():
         if v["launches"] == 0:
             continue
@@ -121,6 +123,7 @@ def run_workload(P, wi, cfg, weights, name, steps, warmup, profile_dominant=True
     dec_s = time.perf_counter() - t1
     model.close()
     return {"elapsed": elapsed, "dominant": dom, "kernels": kernels,
+            "step_flops": step_flops, "step_bytes": step_bytes,
             "decode": {"forwards": forwards, "seconds": round(dec_s, 4),
                        "tokens_per_s": round(B * g / dec_s, 2),
                        "steps_per_seq_mean": sum(seq_steps) / len(seq_steps)}}
@@ -155,6 +158,40 @@ def run_baselines(P, wi, cfg, weights, name, ms=(1, 4)):
         b["wino_tps_speedup"] = round(w["tokens_per_s"] / b["tokens_per_s"], 3)
     out["workload"] = f"{preset} decode, batch {B}, prompt {p}, gen {g}, block {lb}, tau1 {tau1}, tau2 {tau2}"
     return out
+
+
+def run_epilogue(P, wi, n_calls=20, n_buf=4):
+    """Standalone WINO epilogue on given bf16 logits [8, 64, 126464] (the
+    decision of Eq. 2-4 read from materialised logits), timed with HIP events
+    over n_calls calls rotating n_buf logit buffers (more bytes than the 256 MB
+    Infinity Cache holds), each call on a fresh copy of the block state."""
+    import torch
+    B, lb, V, mask = 8, 32, 126464, 126463
+    bufs, curs = [], []
+    for i in range(n_buf):
+        lg, cur, _ = wi.epilogue_inputs(B, lb, V, mask, seed=2 + 100 * i, device="cuda")
+        bufs.append(lg)
+        curs.append(cur)
+    states = [curs[i % n_buf].clone() for i in range(n_calls)]
+    prm = P.make_params(B, 1, lb, lb, mask, 0.7, 0.9)
+    ws_bytes = P.wino_epilogue_workspace_bytes(B, lb, V)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    bitmap = torch.empty(B, lb, dtype=torch.uint8, device="cuda")
+    for i in range(2):
+        P.wino_epilogue(prm, V, bufs[i % n_buf], curs[i % n_buf].clone(), bitmap, workspace=ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(n_calls):
+        P.wino_epilogue(prm, V, bufs[i % n_buf], states[i], bitmap, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / n_calls
+    algo = B * lb * V * 2  # one bf16 row per position is read (Eq. 4)
+    return {"workload": f"standalone epilogue, logits [{B}, {2 * lb}, {V}] bf16, {n_buf} rotating buffers",
+            "ms_per_call": round(ms, 4), "algorithmic_bytes": algo,
+            "gbs": round(algo / (ms * 1e-3) / 1e9, 1),
+            "hbm_frac": round(algo / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
 
 
 def cpu_baseline(wi, cfg, weights, name):
@@ -274,15 +311,25 @@ def main():
                      "traffic": measured_traffic(), "avg_launch_ms": round(dom_ms, 4),
                      "flops_per_launch": dom_flops, "launches": dom["launches"]},
         "kernels": res["kernels"],
+        # algorithmic work of one step (sum over its kernels) at the MI355X
+        # peaks: the step's floor time, and how far the measured step is from it
+        "step_floor": {"flops": res["step_flops"], "bytes": res["step_bytes"],
+                       "mfma_ms": round(res["step_flops"] / (PEAK_BF16_TFLOPS * 1e12) * 1e3, 3),
+                       "hbm_ms": round(res["step_bytes"] / (PEAK_HBM_GBS * 1e9) * 1e3, 3),
+                       "frac_of_mfma_floor": round(res["step_flops"] / (PEAK_BF16_TFLOPS * 1e12) * 1e3 / ms, 4)},
     }
     if a.config == "bs16" and not a.no_bs1:
         log("bs1 workload")
         r1 = run_workload(P, wi, cfg, weights, "bs1", a.steps, a.warmup)
         ms1 = r1["elapsed"] / a.steps * 1e3
         line["bs1"] = {"steps_per_s": round(1e3 / ms1, 3), "ms_per_step": round(ms1, 3),
+                       "step_floor": {"mfma_ms": round(r1["step_flops"] / (PEAK_BF16_TFLOPS * 1e12) * 1e3, 3),
+                                      "hbm_ms": round(r1["step_bytes"] / (PEAK_HBM_GBS * 1e9) * 1e3, 3)},
                        "tokens_per_s": r1["decode"]["tokens_per_s"], "decode": r1["decode"],
                        "kernels": r1["kernels"]}
     if a.config == "bs16" and not a.no_bs1:
+        log("standalone epilogue")
+        line["epilogue"] = run_epilogue(P, wi)
         log("baseline decoders (bs1)")
         line["baselines"] = run_baselines(P, wi, cfg, weights, "bs1")
     if not a.no_cpu_baseline:
