@@ -61,7 +61,7 @@ def make_state(wi, cfg, B, p, g, lb, image_prefix, seed=1000):
     return tok.contiguous(), block_start
 
 
-def run_workload(P, wi, cfg, weights, name, steps, warmup, profile_dominant=True):
+def run_workload(P, wi, cfg, weights, name, steps, warmup, profile_dominant=True, decode=True):
     import torch
     preset, B, p, g, lb, tau1, tau2, img = CONFIGS[name]
     model = P.WinoModel(cfg, weights, B, p + g + lb)
@@ -113,6 +113,10 @@ def run_workload(P, wi, cfg, weights, name, steps, warmup, profile_dominant=True
                       "tflops": round(v["flops"] / 2 / (ms * 1e-3) / 1e12, 2) if v["flops"] else None,
                       "gbs": round(v["bytes"] / 2 / (ms * 1e-3) / 1e9, 1) if v["bytes"] else None}
 
+    if not decode:
+        model.close()
+        return {"elapsed": elapsed, "dominant": dom, "kernels": kernels,
+                "step_flops": step_flops, "step_bytes": step_bytes, "decode": None}
     # full decode from the prompt: generated tokens per second
     pr_tok = wi.initial_tokens(wi.prompts(cfg, B, p, seed=1000, image_prefix=img), g, cfg.mask_id).cuda()
     dbs = torch.zeros(B, dtype=torch.int32, device="cuda")
@@ -259,6 +263,8 @@ def main():
     ap.add_argument("--config", default="bs16", choices=sorted(CONFIGS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bs1", action="store_true")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="skip the full decode (kernel profiles of the step shape only)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run plain device copies of known size (HBM counter calibration)")
     a = ap.parse_args()
@@ -289,7 +295,7 @@ def main():
         del src, dst
         log("copy calibration done (3 x 512 MiB)")
 
-    res = run_workload(P, wi, cfg, weights, a.config, a.steps, a.warmup)
+    res = run_workload(P, wi, cfg, weights, a.config, a.steps, a.warmup, decode=not a.no_decode)
     _, B, p, g, lb, tau1, tau2, img = CONFIGS[a.config]
     ms = res["elapsed"] / a.steps * 1e3
     dom = res["dominant"]
@@ -304,7 +310,7 @@ def main():
         "config": {"workload": f"{preset} WINO step, batch {B}, prompt {p}, gen {g}, block {lb}",
                    "batch": B, "prompt_len": p, "gen_len": g, "block_len": lb, "tau1": tau1,
                    "tau2": tau2, "init": "literal (LM head std 0.5/sqrt(d), Zipf bias)"},
-        "tokens_per_s": res["decode"]["tokens_per_s"],
+        "tokens_per_s": res["decode"]["tokens_per_s"] if res["decode"] else None,
         "decode": res["decode"],
         "roofline": {"bound": "mfma", "kernel": DOMINANT, "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
