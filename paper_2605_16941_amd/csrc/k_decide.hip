@@ -33,9 +33,9 @@ __device__ __forceinline__ void merge(Part& a, const Part& o) {
   a.t = fmaxf(a.t, o.t);
 }
 
-__device__ __forceinline__ Part wave_merge(Part p) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
+// Merge across aligned groups of gs lanes (gs a power of two <= 64).
+__device__ __forceinline__ Part group_merge(Part p, int gs) {
+  for (int o = gs >> 1; o > 0; o >>= 1) {
     Part q;
     q.m = __shfl_xor(p.m, o, 64);
     q.s = __shfl_xor(p.s, o, 64);
@@ -55,7 +55,7 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
   int* s_flag = s_hat + a.Lb;                             // [Lb] decision
   __shared__ int s_nmask, s_nmask_after, s_any_draft, s_forced;
 
-  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int b = blockIdx.x, tid = threadIdx.x;
   const int Lb = a.Lb;
   RowStats* stats = reinterpret_cast<RowStats*>(a.stats);
 
@@ -98,17 +98,25 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
     return;
   }
 
-  // merge partials: one wave per position
-  for (int l = wave; l < Lb; l += 4) {
-    const size_t row = (size_t)b * Lb + l;
+  // merge partials: a group of gs lanes per position, every position of a
+  // pass at once (gs * positions = 256), so the partial loads of all
+  // positions are in flight together
+  int gs = 1;
+  while (gs < 64 && gs * 2 * Lb <= 256) gs *= 2;
+  const int per_pass = 256 / gs;
+  for (int base = 0; base < Lb; base += per_pass) {
+    const int l = base + tid / gs, sl = tid & (gs - 1);
+    const size_t row = (size_t)b * Lb + (l < Lb ? l : 0);
     Part p = {kNegBig, 0.f, kNegBig, kNegBig, INT_MAX};
-    for (int j = lane; j < a.n_part; j += 64) {
-      const size_t o = row * a.n_part + j;
-      Part q = {a.pm[o], a.ps[o], a.pb[o], a.pt[o], a.pi[o]};
-      merge(p, q);
+    if (l < Lb) {
+      for (int j = sl; j < a.n_part; j += gs) {
+        const size_t o = row * a.n_part + j;
+        Part q = {a.pm[o], a.ps[o], a.pb[o], a.pt[o], a.pi[o]};
+        merge(p, q);
+      }
     }
-    p = wave_merge(p);
-    if (lane == 0) {
+    p = group_merge(p, gs);
+    if (sl == 0 && l < Lb) {
       const bool masked = s_cur[l] == a.mask_id;
       const float z = masked ? p.b : p.t;
       s_val[l] = __expf(z - p.m) / p.s;  // Eq. 2 confidence / Eq. 3 probability
