@@ -153,6 +153,68 @@ def test_residual_stream_matches_oracle(P, n_sub):
     assert max(errs16) < 3 * chaos + 1e-4
 
 
+@pytest.mark.parametrize("p,g,lb,B", [(0, 21, 7, 3), (6, 24, 3, 2), (13, 20, 20, 1)])
+def test_ragged_shapes_forward_and_decode(P, p, g, lb, B):
+    """Ragged edge cases: no prompt, T = P + G + L_b not a multiple of 8 (the
+    QKV epilogue's element stores for v^T runs that cross a sequence end), an
+    odd block length, and a single block spanning the whole response.  The
+    full-depth residual stream must match the oracle as closely as the
+    oracle's own sensitivity to float32-level noise allows, and a decode must agree
+    with the oracle's wherever its decisions are robust."""
+    cfg, w = tiny("wide", seed=2)
+    wd = to_device(w)
+    T = p + g + lb
+    model = P.WinoModel(cfg, wd, B, T)
+    tok = batch_tokens(cfg, B, p, g, seed=4, fill=[(0, lb, 0.5)]) if p > 0 else \
+        np.full((B, g), cfg.mask_id, dtype=np.int64)
+    if p == 0:
+        rng = np.random.default_rng(4)
+        first = rng.random((B, lb)) < 0.5
+        tok[:, :lb][first] = rng.integers(0, cfg.mask_id, int(first.sum()))
+    bstart = [0] * B
+    prm = P.make_params(B, p, g, lb, cfg.mask_id)
+    n_sub = 2 * cfg.n_layers
+    out = torch.empty(B, T, cfg.d_model, dtype=torch.float32, device="cuda")
+    P.wino_debug_forward(model.ctx, prm, torch.tensor(tok, dtype=torch.int32, device="cuda"),
+                         torch.tensor(bstart, dtype=torch.int32, device="cuda"), n_sub, out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    # The bf16-point oracle's sensitivity is a step function: an input change
+    # either flips no bf16 rounding (error ~ the change) or flips one (~1e-3).
+    # Float32 accumulation-order differences over a K-long dot product reach
+    # ~sqrt(K) * 2^-24 ~ 1e-6 relative, so the noise is probed at 1e-7 and 1e-6.
+    chaos, errs16 = 0.0, []
+    for b in range(B):
+        ext, pos, allowed, _ = M.extended_inputs(tok[b], p, g, lb, bstart[b], cfg.mask_id)
+        ref = oracle_rows(w, cfg, ext, pos, allowed, n_sub)
+        ref16 = oracle_rows(w, cfg, ext, pos, allowed, n_sub, M.round_bf16)
+        for eps in (1e-7, 1e-6):
+            for seed in (1, 2):
+                chaos = max(chaos, rowwise_rel_err(oracle_rows(w, cfg, ext, pos, allowed, n_sub, M.round_bf16,
+                                                               perturb=eps, seed=seed), ref16))
+        assert rowwise_rel_err(got[b], ref) < 1e-2
+        errs16.append(rowwise_rel_err(got[b], ref16))
+    print(f"T={T}: vs bf16-point {max(errs16):.2e}, oracle self-sensitivity {chaos:.2e}")
+    assert max(errs16) < 3 * chaos + 1e-4
+    # decode from all-mask responses with the same prompts
+    tok0 = tok.copy()
+    tok0[:, p:] = cfg.mask_id
+    dt = torch.tensor(tok0, dtype=torch.int32, device="cuda")
+    bs = torch.zeros(B, dtype=torch.int32, device="cuda")
+    steps, forwards = P.wino_decode(model.ctx, prm, dt, bs)
+    torch.cuda.synchronize()
+    dgot = dt.cpu().numpy()
+    assert not np.any(dgot[:, p:] == cfg.mask_id) and np.array_equal(dgot[:, :p], tok0[:, :p])
+    oprm = oracle_params(prm)
+    prov = W.ModelProvider(w, cfg, act_round=M.round_bf16)
+    for b in range(B):
+        traj, final = oracle_trajectory(prov, tok0[b], oprm)
+        if robust_trajectory(traj, p, lb, cfg.mask_id):
+            assert np.array_equal(dgot[b], final), f"seq {b}: decode differs from the oracle"
+            assert steps[b] == len(traj)
+    model.close()
+
+
 def oracle_rows(w, cfg, ext, pos, allowed, n_sub, act_round=None, perturb=0.0, seed=0):
     """Oracle residual after n_sub sublayers, optionally with the embedding
     rows scaled by (1 + perturb * N(0,1)) to expose float32-level sensitivity."""
