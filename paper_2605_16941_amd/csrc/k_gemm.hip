@@ -25,6 +25,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <mutex>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -380,13 +381,16 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
   // Tile order: each XCD takes a contiguous range of logical tiles, walked in
   // groups of GM M-tiles so the ~32 workgroups an XCD runs at once cover
   // GM A tiles x (32/GM) W tiles and reuse both from its L2.
-  // Work units: whole-K tiles of the rows below split_row0 first, then (the
-  // residual epilogue only) `splits` K-slices of each tile above it, so a
-  // last partial round of whole tiles becomes a full round of thin slices.
+  // Work units: whole-K tiles of the full row tiles first, then the rest:
+  // with the residual epilogue and splits > 1, `splits` K-slices of each
+  // tile from split_row0 on (a last partial round of whole tiles becomes a
+  // full round of thin slices); otherwise the partial last row tile, whose
+  // waves past M skip their MFMAs - these finish early, so they go last and
+  // fill the CUs the full tiles leave free.
   constexpr int GM = 8;
   const int nTM = (c.M + BM - 1) / BM, nTN = c.N / BN;
-  const bool has_tail = EPI == EPI_RESIDUAL && c.splits > 1;
-  const int mainTM = has_tail ? c.split_row0 / BM : nTM;
+  const bool ksplit = EPI == EPI_RESIDUAL && c.splits > 1;
+  const int mainTM = ksplit ? c.split_row0 / BM : c.M / BM;
   const int n_main = mainTM * nTN;
   const bool tail = (int)blockIdx.x >= n_main;
   const int tailTM = nTM - mainTM;
@@ -399,16 +403,24 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
   const int gsz = min(rTM - first_m, GM);
   const int tm = (tail ? mainTM : 0) + first_m + (t % (GM * nTN)) % gsz;
   const int tn = (t % (GM * nTN)) / gsz;
-  const int Ku = tail ? c.K / c.splits : c.K;  // K depth of this unit
+  const int Ku = ksplit && tail ? c.K / c.splits : c.K;  // K depth of this unit
   const int m0 = tm * BM, n0 = tn * BN;
 
   // The lane that fills position (lane % CPR) of row RPI*i + lane/CPR of a
   // tile fetches the chunk that belongs there: position ^ lds_swz(row).
   const int lrow = lane / CPR, lpos = lane % CPR;
   const int kbase = split * Ku;  // first K column of this unit
+  // In a partial row tile (8-wave shapes; the 4-wave ones would need more
+  // registers for the extra code paths) a wave skips the MFMAs of its rows
+  // past M and the copies of A rows past M (they feed only output rows past
+  // M); with two stages every later wait is for all of a wave's copies, so
+  // only the first wait changes.
+  constexpr bool CAN_SKIP = NST == 2 && !SPLIT && NW == 8;
+  bool alive[A_INS];
   const uint16_t* asrc[A_INS];
 #pragma unroll
   for (int i = 0; i < A_INS; ++i) {
+    alive[i] = m0 + (wave * A_INS + i) * RPI < c.M;
     const int gi = wave * A_INS + i;
     const int row = gi * RPI + lrow;
     const int lkc = lpos ^ lds_swz<KB>(row);
@@ -426,14 +438,15 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
     bsrc[i] = c.W + (size_t)wr * c.ldw + kbase + lkc * 8;
   }
 
-  auto issue = [&](int kt, int stage) {
+  auto issue = [&](int kt, int stage, auto skip_tag) {
     uint16_t* sA = smem + stage * STAGE;
     uint16_t* sB = sA + AROWS * KB;
 #pragma unroll
     for (int i = 0; i < A_INS; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + kt * KB),
-                                       (__attribute__((address_space(3))) void*)(sA + (wave * A_INS + i) * 512),
-                                       16, 0, 0);
+      if (!decltype(skip_tag)::value || alive[i])
+        __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + kt * KB),
+                                         (__attribute__((address_space(3))) void*)(sA + (wave * A_INS + i) * 512),
+                                         16, 0, 0);
 #pragma unroll
     for (int i = 0; i < B_INS; ++i)
       __builtin_amdgcn_global_load_lds((const void*)(bsrc[i] + kt * KB),
@@ -465,17 +478,25 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
     bswz[fn] = lds_swz<KB>(r);
   }
   constexpr int KS = KB / 16;
-  constexpr int NR = FM + FN + (SPLIT ? FM : 0);   // LDS fragment reads per 16-deep step
-  constexpr int NM = FM * FN * (SPLIT ? 2 : 1);     // MFMAs per step
-  constexpr int RI = NR < NM ? NR : NM;              // reads interleaved with MFMAs
   static_assert(KS % 2 == 0, "fragment buffers alternate per step");
-
   bf16x8 af[2][FM], bf[2][FN], al[2][SPLIT ? FM : 1];
+
+  // The K loop for a wave whose first FMV of its FM 32-row blocks hold rows
+  // below M (FMV = FM everywhere but in a partial last row tile): the other
+  // blocks' fragment reads and MFMAs are skipped; the wave still issues its
+  // share of the tile copies and meets every barrier.
+  auto pipeline = [&](auto fmv_tag, auto skip_tag) {
+  constexpr int FMV = decltype(fmv_tag)::value;
+  constexpr bool SKIP = decltype(skip_tag)::value;
+  constexpr int NR = FMV ? FMV + FN + (SPLIT ? FMV : 0) : 0;  // LDS fragment reads per 16-deep step
+  constexpr int NM = FMV * FN * (SPLIT ? 2 : 1);              // MFMAs per step
+  constexpr int RI = NR < NM ? NR : NM;                       // reads interleaved with MFMAs
   auto load_frags = [&](const uint16_t* sA, int ks, int buf) {
+    if constexpr (FMV > 0) {
     const uint16_t* sB = sA + AROWS * KB;
     const int kc = ks * 2 + (lane >> 5);
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm)
+    for (int fm = 0; fm < FMV; ++fm)
       af[buf][fm] = as_bf16x8(*reinterpret_cast<const uint4*>(
           sA + (arow + fm * 32) * KB + ((kc ^ aswz[fm]) << 3)));
 #pragma unroll
@@ -484,19 +505,20 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
           sB + (brow + fn * 32) * KB + ((kc ^ bswz[fn]) << 3)));
     if constexpr (SPLIT) {
 #pragma unroll
-      for (int fm = 0; fm < FM; ++fm)
+      for (int fm = 0; fm < FMV; ++fm)
         al[buf][fm] = as_bf16x8(*reinterpret_cast<const uint4*>(
             sA + (BM + arow + fm * 32) * KB + ((kc ^ alswz[fm]) << 3)));
+    }
     }
   };
   auto mfmas = [&](int buf) {
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm)
+    for (int fm = 0; fm < FMV; ++fm)
 #pragma unroll
       for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma32(af[buf][fm], bf[buf][fn], acc[fm][fn]);
     if constexpr (SPLIT) {
 #pragma unroll
-      for (int fm = 0; fm < FM; ++fm)
+      for (int fm = 0; fm < FMV; ++fm)
 #pragma unroll
         for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma32(al[buf][fm], bf[buf][fn], acc[fm][fn]);
     }
@@ -508,6 +530,7 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
       load_frags(sA, ks + 1, (ks + 1) & 1);
       mfmas(ks & 1);
     }
+    if constexpr (NR > 0) {
 #pragma unroll
     for (int ks = 0; ks + 1 < KS; ++ks) {
 #pragma unroll
@@ -517,6 +540,7 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
       }
       if (NR > RI) __builtin_amdgcn_sched_group_barrier(0x100, NR - RI, 0);
       if (NM > RI) __builtin_amdgcn_sched_group_barrier(0x008, NM - RI, 0);
+    }
     }
   };
 
@@ -529,8 +553,10 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
   // last MFMAs of tile t, which cover the latency of those reads.  Tiles past
   // the end are refetches of the last one, which keeps the wait counts fixed.
 #pragma unroll
-  for (int s0 = 0; s0 < NST; ++s0) issue(s0 < nk ? s0 : nk - 1, s0);
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NST - 1) * INS) : "memory");
+  for (int s0 = 0; s0 < NST; ++s0) issue(s0 < nk ? s0 : nk - 1, s0, skip_tag);
+  // (a wave that may have skipped copies has fewer in flight: it waits for all)
+  if constexpr (SKIP) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NST - 1) * INS) : "memory");
   __syncthreads();
   load_frags(smem, 0, 0);
   int cur = 0;  // stage of tile kt
@@ -538,15 +564,31 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
     inner_steps(smem + cur * STAGE);
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NST - 2) * INS) : "memory");
     __syncthreads();
-    issue(kt + NST < nk ? kt + NST : nk - 1, cur);
+    issue(kt + NST < nk ? kt + NST : nk - 1, cur, skip_tag);
     cur = cur + 1 == NST ? 0 : cur + 1;
     load_frags(smem + cur * STAGE, 0, 0);
     mfmas((KS - 1) & 1);
-    __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+    if constexpr (NR > 0) {
+      __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+    }
   }
   inner_steps(smem + cur * STAGE);
   mfmas((KS - 1) & 1);
+  };  // pipeline
+
+  using Full = std::integral_constant<int, FM>;
+  using Keep = std::false_type;
+  const int vrows = c.M - (m0 + wm * WTM);  // rows of this wave's tile below M
+  if constexpr (CAN_SKIP) {
+    using Skip = std::true_type;
+    if (m0 + BM <= c.M) pipeline(Full{}, Keep{});
+    else if (vrows <= 0) pipeline(std::integral_constant<int, 0>{}, Skip{});
+    else if (FM > 1 && vrows <= 32) pipeline(std::integral_constant<int, 1>{}, Skip{});
+    else pipeline(Full{}, Skip{});
+  } else {
+    pipeline(Full{}, Keep{});
+  }
   // the refetch issued last may still be landing: finish it before the
   // epilogue reuses LDS
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -554,7 +596,7 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
 
   const int rowb = m0 + wm * WTM, colb = n0 + wn * WTN;
   if constexpr (EPI == EPI_RESIDUAL) {
-    if (!tail) epi_residual<FM, FN>(c, acc, rowb, colb, lane);
+    if (!(ksplit && tail)) epi_residual<FM, FN>(c, acc, rowb, colb, lane);
     else epi_partial<FM, FN>(c, acc, rowb, colb, lane, split);
   }
   else if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_LOGITS) epi_store<FM, FN>(c, acc, rowb, colb, lane);
@@ -582,7 +624,11 @@ struct TileCfg {
 // Entry 9 gives the QKV GEMM (a head per wave) two waves per SIMD at few
 // rows: 678 vs 598 TFLOP/s at 544 rows.  Entry 4 is set from the 544-row O
 // projection (split 2: 40.8 us against 34.6 us for entry 3), where its three
-// workgroups per CU are rarely all resident.
+// workgroups per CU are rarely all resident.  Entry 10 keeps two K tiles in
+// flight instead of one: at 544 rows each weight strip is read by few row
+// tiles, so most of its copies miss L2, and the QKV GEMM takes 66 instead
+// of 74 us (weights streamed from HBM); where the weights are shared by many
+// row tiles the third stage does not pay (deeper pipelines lost there).
 constexpr TileCfg kTiles[] = {
     {256, 256, 2, 2, 64, 2, 1, 0.95f},  // 0
     {192, 256, 2, 2, 64, 2, 1, 0.75f},  // 1
@@ -594,6 +640,7 @@ constexpr TileCfg kTiles[] = {
     {256, 256, 2, 4, 64, 2, 1, 0.98f},  // 7  (8 waves)
     {128, 256, 2, 4, 64, 2, 1, 0.74f},  // 8  (8 waves)
     {128, 256, 4, 2, 64, 2, 1, 0.77f},  // 9  (8 waves, 32-row wave tiles)
+    {128, 256, 4, 2, 64, 3, 1, 0.78f},  // 10 (8 waves, three stages)
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 
@@ -630,18 +677,6 @@ int env_int(const char* name, int dflt) {
 // workgroups it holds; epilogue traffic moves at ~4 TB/s shared by all slots.
 constexpr double kCuFlops = 6.5e12, kEpiBw = 4.0e12, kPartBw = 2.5e12;
 
-// Estimated seconds for whole-K tiles: waves of workgroups over 256 CUs (a CU
-// holding fewer tiles than it could runs proportionally less efficiently).
-double tile_time(const GemmCall& c, const TileCfg& t) {
-  const long tiles = (long)((c.M + t.BM - 1) / t.BM) * (c.N / t.BN);
-  const long slots = 256L * t.occ;
-  const long rounds = (tiles + slots - 1) / slots;
-  const long per_cu = std::min<long>(t.occ, (tiles + 255) / 256);
-  const double util = 0.5 + 0.5 * (double)per_cu / t.occ;
-  const double tile_s = 2.0 * t.BM * t.BN * (double)c.K / (t.eff * util * kCuFlops);
-  return rounds * per_cu * tile_s;
-}
-
 // Makespan of n_main jobs of length T followed by n_units jobs of length U,
 // each started on the slot that frees first (the hardware dispatcher's order).
 double makespan(long n_main, double T, long n_units, double U, long slots) {
@@ -666,6 +701,39 @@ double makespan(long n_main, double T, long n_units, double U, long slots) {
   return std::max(main_end, best);
 }
 
+// Time of the partial last row tile (rem = M mod BM rows) relative to a full
+// one.  8-wave shapes skip the MFMAs of rows past M per wave (the kernel's
+// rule: a wave keeps all its 32-row blocks, only the first, or none), so the
+// busiest SIMD's remaining share sets the time, floored at kPartialFloor for
+// the copies and barriers every wave still makes.  Other shapes: a full tile.
+constexpr double kPartialFloor = 0.3;
+double partial_share(const GemmCall& c, const TileCfg& t, int rem) {
+  const bool lm = c.epi == EPI_LMSTATS || c.epi == EPI_LOGITS;
+  if (rem == 0 || lm || t.WM * t.WN != 8 || t.NST != 2) return 1.0;
+  const int WTM = t.BM / t.WM, FM = WTM / 32;
+  double load[4] = {0, 0, 0, 0};
+  for (int w = 0; w < 8; ++w) {
+    const int v = rem - (w / t.WN) * WTM;
+    const int fmv = v <= 0 ? 0 : (FM > 1 && v <= 32 ? 1 : FM);
+    load[w % 4] += (double)fmv / FM;
+  }
+  const double busiest = std::max(std::max(load[0], load[1]), std::max(load[2], load[3])) / 2.0;
+  return std::max(busiest, kPartialFloor);
+}
+
+// Estimated seconds for whole-K tiles: the full row tiles, then the partial
+// last row tile (the kernel's order), dealt to 256 CUs as they free up (a CU
+// holding fewer tiles than it could runs proportionally less efficiently).
+double tile_time(const GemmCall& c, const TileCfg& t) {
+  const long nTN = c.N / t.BN;
+  const int rem = c.M % t.BM;
+  const long n_full = (long)(c.M / t.BM) * nTN, n_part = rem ? nTN : 0;
+  const long per_cu = std::min<long>(t.occ, (n_full + n_part + 255) / 256);
+  const double util = 0.5 + 0.5 * (double)per_cu / t.occ;
+  const double tile_s = 2.0 * t.BM * t.BN * (double)c.K / (t.eff * util * kCuFlops);
+  return makespan(n_full, tile_s, n_part, partial_share(c, t, rem) * tile_s, 256);
+}
+
 // Residual GEMM: whole-K tiles read-add-write 8 bytes of x per output; the
 // `splits` K-slices of the last tail_tm row tiles write 4-byte partials that
 // the next norm kernel reads back.
@@ -676,7 +744,10 @@ double residual_time(const GemmCall& c, const TileCfg& t, int tail_tm, int split
   const double out_s = (double)t.BM * t.BN / (kEpiBw / slots);
   const double T = 2.0 * t.BM * t.BN * (double)c.K / rate + 8.0 * out_s;
   const long n_main = (long)(nTM - tail_tm) * nTN;
-  if (tail_tm == 0) return makespan(n_main, T, 0, 0, slots);
+  if (tail_tm == 0) {
+    const int rem = c.M % t.BM;
+    return makespan(n_main - (rem ? nTN : 0), T, rem ? nTN : 0, partial_share(c, t, rem) * T, slots);
+  }
   const double U = 2.0 * t.BM * t.BN * ((double)c.K / splits + 2 * BK) / rate + 4.0 * out_s;
   const long n_units = (long)tail_tm * nTN * splits;
   const double tail_rows = c.M - (double)(nTM - tail_tm) * t.BM;
@@ -809,6 +880,7 @@ hipError_t launch_gemm(const GemmCall& c, hipStream_t st) {
     case 7: return launch_cfg<256, 256, 2, 4, 64, 2, 1>(c, st);
     case 8: return launch_cfg<128, 256, 2, 4, 64, 2, 1>(c, st);
     case 9: return launch_cfg<128, 256, 4, 2, 64, 2, 1>(c, st);
+    case 10: return launch_cfg<128, 256, 4, 2, 64, 3, 1>(c, st);
   }
   return hipErrorInvalidValue;
 }
