@@ -109,10 +109,19 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
     const size_t row = (size_t)b * Lb + (l < Lb ? l : 0);
     Part p = {kNegBig, 0.f, kNegBig, kNegBig, INT_MAX};
     if (l < Lb) {
-      for (int j = sl; j < a.n_part; j += gs) {
-        const size_t o = row * a.n_part + j;
-        Part q = {a.pm[o], a.ps[o], a.pb[o], a.pt[o], a.pi[o]};
-        merge(p, q);
+      // eight partials' loads in flight per lane before they are merged
+      constexpr int U = 8;
+      for (int j0 = sl; j0 < a.n_part; j0 += gs * U) {
+        Part q[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int j = j0 + u * gs;
+          const size_t o = row * a.n_part + (j < a.n_part ? j : 0);
+          q[u] = Part{a.pm[o], a.ps[o], a.pb[o], a.pt[o], a.pi[o]};
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          if (j0 + u * gs < a.n_part) merge(p, q[u]);
       }
     }
     p = group_merge(p, gs);
@@ -154,13 +163,20 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
     s_flag[l] = f;
   }
   __syncthreads();
-  if (tid == 0 && a.topm == 0 && !cap_now && a.force_top1 && s_nmask > 0 && !s_any_draft) {
-    // Eq. 1: the most confident masked position (lowest position on ties)
-    int best = -1;
-    float bv = 0.f;
-    for (int l = 0; l < Lb; ++l)
-      if (s_cur[l] == a.mask_id && (best < 0 || s_val[l] > bv)) { best = l; bv = s_val[l]; }
-    s_flag[best] = WINO_FORCED_FLAG;
+  if (tid < 64 && a.topm == 0 && !cap_now && a.force_top1 && s_nmask > 0 && !s_any_draft) {
+    // Eq. 1: the most confident masked position (lowest position on ties),
+    // one wave: per-lane scan, then a shuffle reduction
+    int best = INT_MAX;
+    float bv = kNegBig;
+    for (int l = tid; l < Lb; l += 64)
+      if (s_cur[l] == a.mask_id && (best == INT_MAX || s_val[l] > bv)) { best = l; bv = s_val[l]; }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(bv, o, 64);
+      const int ob = __shfl_xor(best, o, 64);
+      if (ob != INT_MAX && (best == INT_MAX || ov > bv || (ov == bv && ob < best))) { bv = ov; best = ob; }
+    }
+    if (tid == 0) s_flag[best] = WINO_FORCED_FLAG;
   }
   __syncthreads();
   const int step_no = fin_ptr ? a.seq_steps[b] + 1 : 0;
@@ -235,8 +251,13 @@ __global__ __launch_bounds__(256) void epi_stats_kernel(const uint16_t* __restri
                                                         const int32_t* __restrict__ cur, int Lb, int V,
                                                         int mask_id, float* pm, float* ps, float* pb,
                                                         int32_t* pi, float* pt, int n_part) {
+  // Per logit the common path costs a conversion, a max, and one FMA + exp2
+  // + add for the sum; the best non-mask id is looked up afterwards only by
+  // the threads whose maximum equals the chunk's, the mask id is excluded
+  // only by the thread that holds it, and the target logit is one load.
   constexpr int IT = kEpiChunk / (256 * 8);
-  __shared__ float red[4][4];
+  constexpr float kLog2e = 1.4426950408889634f;
+  __shared__ float red[3][4];
   __shared__ int redi[4];
   const int r = blockIdx.y, chunk = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = r / Lb, l = r - b * Lb;
@@ -251,57 +272,62 @@ __global__ __launch_bounds__(256) void epi_stats_kernel(const uint16_t* __restri
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
     const int idx = v0 + (it * 256 + tid) * 8;
-    raw[it] = idx < v1 ? *reinterpret_cast<const uint4*>(row + idx) : make_uint4(0, 0, 0, 0);
+    raw[it] = idx < v1 ? *reinterpret_cast<const uint4*>(row + idx) : make_uint4(0xFF7FFF7Fu, 0xFF7FFF7Fu, 0xFF7FFF7Fu, 0xFF7FFF7Fu);
   }
-  float mx = kNegBig, bz = kNegBig, tz = kNegBig;
-  int bi = INT_MAX;
+  // (ids past V read as the most negative finite bf16 and never win)
+  auto elem = [&](int it, int e) {
+    const uint32_t w = (&raw[it].x)[e >> 1];
+    return __uint_as_float((e & 1) ? (w & 0xFFFF0000u) : (w << 16));
+  };
+  float mx = kNegBig;
 #pragma unroll
-  for (int it = 0; it < IT; ++it) {
-    const int idx = v0 + (it * 256 + tid) * 8;
-    if (idx >= v1) continue;
-    const uint16_t* p = reinterpret_cast<const uint16_t*>(&raw[it]);
+  for (int it = 0; it < IT; ++it)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float z = bf2f(p[e]);
-      mx = fmaxf(mx, z);
-      if (idx + e != mask_id && z > bz) { bz = z; bi = idx + e; }
-      if (idx + e == tgt) tz = z;
-    }
+    for (int e = 0; e < 8; ++e) mx = fmaxf(mx, elem(it, e));
+  // best value over non-mask ids: differs from mx only in the thread holding mask_id
+  float nm = mx;
+  const int my0 = v0 + tid * 8;  // this thread's ids: my0 + it*2048 + e
+  if (mask_id >= v0 && mask_id < v1 && (mask_id - my0) >= 0 && ((mask_id - my0) & 2047) < 8) {
+    nm = kNegBig;
+#pragma unroll
+    for (int it = 0; it < IT; ++it)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (my0 + it * 2048 + e != mask_id) nm = fmaxf(nm, elem(it, e));
   }
-  // block max
-  float m = wave_max(mx);
-  if (lane == 0) red[0][wave] = m;
+  float m = wave_max(mx), bz = wave_max(nm);
+  if (lane == 0) { red[0][wave] = m; red[1][wave] = bz; }
   __syncthreads();
   m = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
+  bz = fmaxf(fmaxf(red[1][0], red[1][1]), fmaxf(red[1][2], red[1][3]));
+  // lowest non-mask id holding bz (ids grow with it, then e, within a thread)
+  int bi = INT_MAX;
+  if (nm == bz) {
+#pragma unroll
+    for (int it = IT - 1; it >= 0; --it)
+#pragma unroll
+      for (int e = 7; e >= 0; --e) {
+        const int id = my0 + it * 2048 + e;
+        if (id < v1 && id != mask_id && elem(it, e) == bz) bi = id;
+      }
+  }
+  const float mc = m * kLog2e;
   float se = 0.f;
 #pragma unroll
-  for (int it = 0; it < IT; ++it) {
-    const int idx = v0 + (it * 256 + tid) * 8;
-    if (idx >= v1) continue;
-    const uint16_t* p = reinterpret_cast<const uint16_t*>(&raw[it]);
+  for (int it = 0; it < IT; ++it)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) se += __expf(bf2f(p[e]) - m);
-  }
+    for (int e = 0; e < 8; ++e) se += exp2f(fmaf(elem(it, e), kLog2e, -mc));
   se = wave_sum(se);
-  tz = wave_max(tz);
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ob = __shfl_xor(bz, o, 64);
-    const int oi = __shfl_xor(bi, o, 64);
-    if (ob > bz || (ob == bz && oi < bi)) { bz = ob; bi = oi; }
-  }
-  if (lane == 0) { red[1][wave] = se; red[2][wave] = bz; red[3][wave] = tz; redi[wave] = bi; }
+  for (int o = 32; o > 0; o >>= 1) bi = min(bi, __shfl_xor(bi, o, 64));
+  if (lane == 0) { red[2][wave] = se; redi[wave] = bi; }
   __syncthreads();
   if (tid == 0) {
-    float s = 0.f, bb = kNegBig, tt = kNegBig;
-    int ii = INT_MAX;
-    for (int w = 0; w < 4; ++w) {
-      s += red[1][w];
-      tt = fmaxf(tt, red[3][w]);
-      if (red[2][w] > bb || (red[2][w] == bb && redi[w] < ii)) { bb = red[2][w]; ii = redi[w]; }
-    }
+    const float s = (red[2][0] + red[2][1]) + (red[2][2] + red[2][3]);
+    const int ii = min(min(redi[0], redi[1]), min(redi[2], redi[3]));
+    const float tt = tgt >= v0 && tgt < v1 ? bf2f(row[tgt]) : kNegBig;
     const size_t o = (size_t)r * n_part + chunk;
-    pm[o] = m; ps[o] = s; pb[o] = bb; pi[o] = ii; pt[o] = tt;
+    pm[o] = m; ps[o] = s; pb[o] = bz; pi[o] = ii; pt[o] = tt;
   }
 }
 
