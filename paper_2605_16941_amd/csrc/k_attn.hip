@@ -127,6 +127,10 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
   float mrun = kNegBig, lrun = 0.f;
 
   const bool has_shadow = CQ ? g.Ls > 0 && q0 + NW * 32 > g.Lb : min(q0 + NW * 32, g.T) - 1 >= g.S;
+  // A wave whose 32 query rows all lie past the last one (the tail of the
+  // last query tile) only copies tiles and meets the barriers: its SIMD is
+  // left to the other workgroup's wave.
+  const bool wave_live = q0 + wave * 32 < (CQ ? NQ : g.T);
   const int kend = has_shadow ? g.T : g.S;  // shadow rows also see keys S..T-1
   const int ntile = (kend + BKV - 1) / BKV;
 
@@ -153,6 +157,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     if (t + 1 < ntile) issue(kv0 + BKV, (t + 1) & 1);
+    if (!wave_live) continue;
     const uint16_t* sK = smem + (t & 1) * STAGE;
     const uint16_t* sV = sK + KTILE;
 
