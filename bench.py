@@ -198,6 +198,35 @@ def run_epilogue(P, wi, n_calls=20, n_buf=4):
             "hbm_frac": round(algo / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
 
 
+def run_other_configs(P, wi, steps, warmup, names=("mmada", "tiny")):
+    """The remaining workload configurations on their own weights: the
+    MMaDA-shaped long step (vocabulary 134656, batch 4, prompt and response
+    1024, block 64) and the tiny model; step rate, step floors and full-decode
+    tokens/s for each."""
+    import torch
+    out = {}
+    for name in names:
+        preset, B, p, g, lb, tau1, tau2, img = CONFIGS[name]
+        cfg = wi.preset(preset)
+        weights = wi.model_weights(cfg, seed=0, device="cuda")
+        torch.cuda.synchronize()
+        n = steps if cfg.n_layers > 2 else 10 * steps
+        r = run_workload(P, wi, cfg, weights, name, n, warmup, profile_dominant=False)
+        ms = r["elapsed"] / n * 1e3
+        out[name] = {"workload": f"{preset} WINO step, batch {B}, prompt {p}"
+                                 + (f" ({img} image-code ids)" if img else "")
+                                 + f", gen {g}, block {lb}, tau1 {tau1}, tau2 {tau2}, vocab {cfg.vocab}",
+                     "steps_per_s": round(1e3 / ms, 3), "ms_per_step": round(ms, 3),
+                     "tflops": round(r["step_flops"] / (ms * 1e-3) / 1e12, 1),
+                     "step_floor": {"mfma_ms": round(r["step_flops"] / (PEAK_BF16_TFLOPS * 1e12) * 1e3, 3),
+                                    "hbm_ms": round(r["step_bytes"] / (PEAK_HBM_GBS * 1e9) * 1e3, 3)},
+                     "tokens_per_s": r["decode"]["tokens_per_s"], "decode": r["decode"],
+                     "attention_ms_per_step": r["kernels"].get("attention", {}).get("ms_per_step")}
+        del weights
+        torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(wi, cfg, weights, name):
     """The float64 oracle on a bounded sample: one layer of one sequence plus
     the LM head of its block rows, extrapolated to a full batched step."""
@@ -338,6 +367,8 @@ def main():
         line["epilogue"] = run_epilogue(P, wi)
         log("baseline decoders (bs1)")
         line["baselines"] = run_baselines(P, wi, cfg, weights, "bs1")
+        log("other configurations (mmada, tiny)")
+        line["configs"] = run_other_configs(P, wi, a.steps, a.warmup)
     if not a.no_cpu_baseline:
         log("cpu baseline (oracle sample)")
         line["cpu_baseline"] = cpu_baseline(wi, cfg, weights, a.config)
