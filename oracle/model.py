@@ -19,7 +19,9 @@ What WINO itself changes in the forward (Sec. 4.2.2):
 
 Optional ``act_round`` rounds activations at the points where a bf16 pipeline
 materialises them: the normed inputs of the backbone's matrix products, q/k/v
-after RoPE, the attention output and the SwiGLU product.  The final normed
+after RoPE, the unnormalised attention probabilities that multiply v (relative
+to the row maximum; the normalising sum is taken before rounding), the
+attention output and the SwiGLU product.  The final normed
 hidden state feeding the LM head is not rounded (a pipeline that keeps it as a
 hi+lo pair of bf16 values carries 16 mantissa bits there).  With
 ``act_round=None`` everything stays in float64.
@@ -93,10 +95,13 @@ def wino_allowed(seq_len: int, block_len: int, c0: int) -> np.ndarray:
     return a
 
 
-def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, allowed: np.ndarray) -> np.ndarray:
+def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, allowed: np.ndarray,
+              p_round=None) -> np.ndarray:
     """softmax(q k^T / sqrt(hd), restricted to allowed keys) v, per head.
 
-    q, k, v: [T, H, hd]; allowed: [T, T] bool.  Returns [T, H, hd].
+    q, k, v: [T, H, hd]; allowed: [T, T] bool.  Returns [T, H, hd].  With
+    p_round, the unnormalised probabilities exp(s - max) are rounded before
+    they multiply v (the sum that normalises them is not).
     """
     hd = q.shape[-1]
     qh = np.ascontiguousarray(q.transpose(1, 0, 2))
@@ -106,8 +111,10 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, allowed: np.ndarray) 
     s = np.where(allowed[None, :, :], s, -np.inf)
     s = s - np.max(s, axis=-1, keepdims=True)
     p = np.exp(s)
-    p = p / np.sum(p, axis=-1, keepdims=True)
-    return np.matmul(p, vh).transpose(1, 0, 2)
+    l = np.sum(p, axis=-1, keepdims=True)
+    if p_round is not None:
+        p = p_round(p)
+    return (np.matmul(p, vh) / l).transpose(1, 0, 2)
 
 
 def attention_sublayer(x: np.ndarray, lw: dict, cfg, cos, sin, allowed, act_round=None) -> np.ndarray:
@@ -123,7 +130,7 @@ def attention_sublayer(x: np.ndarray, lw: dict, cfg, cos, sin, allowed, act_roun
     q = rnd(apply_rope(q, cos, sin))
     k = rnd(apply_rope(k, cos, sin))
     v = rnd(v)
-    o = rnd(attention(q, k, v, allowed).reshape(t, d))
+    o = rnd(attention(q, k, v, allowed, act_round).reshape(t, d))
     return x + o @ f64(lw["w_o"]).T
 
 

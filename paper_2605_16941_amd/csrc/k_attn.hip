@@ -11,8 +11,8 @@
 // Each wave owns 32 query rows.  Scores are computed transposed, S^T = K Q^T
 // (32x32x16 MFMA), so a lane holds 32 keys of ONE query row and the online
 // softmax max / sum stay inside the lane (plus its partner lane 32 apart).
-// The same registers, split into hi and lo bf16 parts, are the B operand of
-// O^T = V^T P^T.
+// The same registers, rounded to bf16, are the B operand of O^T = V^T P^T
+// (the softmax and its running sum stay in fp32).
 //
 // K and V^T tiles of 64 keys stream global -> LDS by LDS-DMA into two stages
 // (the next tile loads while the current one is used), with 16-byte chunks
@@ -125,6 +125,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
 #pragma unroll
     for (int i = 0; i < 16; ++i) oacc[fe][i] = 0.f;
   float mrun = kNegBig, lrun = 0.f;
+  const float rescale_gap = 8.f / scale_log2;
 
   const bool has_shadow = CQ ? g.Ls > 0 && q0 + NW * 32 > g.Lb : min(q0 + NW * 32, g.T) - 1 >= g.S;
   // A wave whose 32 query rows all lie past the last one (the tail of the
@@ -194,11 +195,23 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
 #pragma unroll
       for (int i = 0; i < 16; ++i) tmax = fmaxf(tmax, s[kb2][i]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    // running max in raw score units; probabilities exp2(s*c - m*c) with
-    // c = log2(e)/sqrt(hd): one FMA per score
-    const float mnew = fmaxf(mrun, tmax);
-    const float alpha = exp2f((mrun - mnew) * scale_log2);
-    const float mc = mnew == kNegBig ? 0.f : mnew * scale_log2;
+    // Reference max mrun in raw score units; probabilities exp2(s*c - m*c)
+    // with c = log2(e)/sqrt(hd): one FMA per score.  The reference moves
+    // (and O, l are rescaled) only when a score exceeds it by more than
+    // 8/c, so probabilities stay below 2^8 and the rescale is rare after
+    // the first tile; p and l share the reference, so O / l is unchanged.
+    const bool resc = tmax > mrun + rescale_gap;
+    if (__any(resc)) {
+      const float mnew = resc ? tmax : mrun;
+      const float alpha = exp2f((mrun - mnew) * scale_log2);
+      lrun *= alpha;
+      mrun = mnew;
+#pragma unroll
+      for (int fe = 0; fe < FE; ++fe)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[fe][i] *= alpha;
+    }
+    const float mc = mrun == kNegBig ? 0.f : mrun * scale_log2;
     float psum = 0.f;
 #pragma unroll
     for (int kb2 = 0; kb2 < 2; ++kb2)
@@ -208,35 +221,24 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
         s[kb2][i] = p;
         psum += p;
       }
-    lrun = lrun * alpha + psum;
-    mrun = mnew;
-#pragma unroll
-    for (int fe = 0; fe < FE; ++fe)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) oacc[fe][i] *= alpha;
+    lrun += psum;
 
 #pragma unroll
     for (int ks4 = 0; ks4 < BKV / 16; ++ks4) {
-      // P as hi + lo bf16 parts: the product with V keeps ~16 mantissa bits
-      // of the probabilities instead of bf16's 8.  Registers 8*(ks4&1)..+7 of
-      // block ks4/2 hold keys 16*ks4 + 8*grp + 0..7.
+      // P in bf16: registers 8*(ks4&1)..+7 of block ks4/2 hold keys
+      // 16*ks4 + 8*grp + 0..7.
       const int base = 8 * (ks4 & 1);
-      uint32_t ph[4], pl[4];
+      uint32_t ph[4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float p0 = s[ks4 >> 1][base + 2 * e], p1 = s[ks4 >> 1][base + 2 * e + 1];
-        ph[e] = pack2bf(p0, p1);
-        pl[e] = pack2bf(p0 - bf2f((uint16_t)(ph[e] & 0xFFFFu)), p1 - bf2f((uint16_t)(ph[e] >> 16)));
-      }
-      const bf16x8 pf_hi = as_bf16x8(make_uint4(ph[0], ph[1], ph[2], ph[3]));
-      const bf16x8 pf_lo = as_bf16x8(make_uint4(pl[0], pl[1], pl[2], pl[3]));
+      for (int e = 0; e < 4; ++e)
+        ph[e] = pack2bf(s[ks4 >> 1][base + 2 * e], s[ks4 >> 1][base + 2 * e + 1]);
+      const bf16x8 pf = as_bf16x8(make_uint4(ph[0], ph[1], ph[2], ph[3]));
 #pragma unroll
       for (int fe = 0; fe < FE; ++fe) {
         const int row = fe * 32 + (lane & 31);
         const int ch = (ks4 * 2 + grp) ^ vswz[fe];
         const bf16x8 vf = as_bf16x8(*reinterpret_cast<const uint4*>(sV + row * BKV + ch * 8));
-        oacc[fe] = mfma32(vf, pf_hi, oacc[fe]);
-        oacc[fe] = mfma32(vf, pf_lo, oacc[fe]);
+        oacc[fe] = mfma32(vf, pf, oacc[fe]);
       }
     }
   }
