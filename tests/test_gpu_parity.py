@@ -570,6 +570,47 @@ def test_row_losses_match_oracle(P, variant):
     model.close()
 
 
+def test_params_rejected_against_the_context(P):
+    """With a live context, parameters the context cannot serve are rejected on
+    the host with the documented status before any device work (batch above
+    max_batch, P + G + L_b above max_seq, L_b not dividing G, a mask id outside
+    the vocabulary, a NaN threshold, a negative tokens_per_step), and the
+    context is unharmed: a valid step afterwards equals a fresh context's."""
+    cfg, w = tiny()
+    wd = to_device(w)
+    p, g, lb, B = 32, 64, 16, 2
+    model = P.WinoModel(cfg, wd, B, p + g + lb)
+    tok = torch.tensor(batch_tokens(cfg, B, p, g, fill=[(0, 16, 0.5)]), dtype=torch.int32, device="cuda")
+    bs = torch.zeros(B, dtype=torch.int32, device="cuda")
+    invalid, shape = -1, -2
+    cases = [(P.make_params(B + 1, p, g, lb, cfg.mask_id), shape),
+             (P.make_params(B, p + 1, g, lb, cfg.mask_id), shape),
+             (P.make_params(B, p, g, 12, cfg.mask_id), shape),
+             (P.make_params(B, p, g, lb, cfg.vocab), invalid),
+             (P.make_params(B, p, g, lb, cfg.mask_id, float("nan")), invalid),
+             (P.make_params(B, p, g, lb, cfg.mask_id, tokens_per_step=-1), invalid)]
+    for prm, want in cases:
+        t = tok.clone()
+        with pytest.raises(P.WinoError) as e:
+            P.wino_step(model.ctx, prm, t, bs)
+        assert e.value.status == want
+        with pytest.raises(P.WinoError) as e:
+            P.wino_decode(model.ctx, prm, t, bs.clone())
+        assert e.value.status == want
+        torch.cuda.synchronize()
+        assert torch.equal(t, tok)
+    prm = P.make_params(B, p, g, lb, cfg.mask_id)
+    t1 = tok.clone()
+    P.wino_step(model.ctx, prm, t1, bs)
+    fresh = P.WinoModel(cfg, wd, B, p + g + lb)
+    t2 = tok.clone()
+    P.wino_step(fresh.ctx, prm, t2, bs)
+    torch.cuda.synchronize()
+    assert torch.equal(t1, t2) and not torch.equal(t1, tok)
+    model.close()
+    fresh.close()
+
+
 def test_step_is_deterministic(P):
     cfg, w = tiny("wide", seed=6)
     wd = to_device(w)
