@@ -48,6 +48,21 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// LDS-DMA of 16 bytes per lane (global_load_lds_dwordx4) into the 1 KB block
+// at l + j KB (j = 0..3): the LDS base goes to M0 and j KB into the
+// instruction's offset, which applies to the global address as well, so g
+// is the source pointer minus j KB.  Up to four consecutive blocks of a wave
+// then share one M0 value; every M0 write costs issue time next to the MFMAs.
+__device__ __forceinline__ void dma16(const uint16_t* g, uint16_t* l, int j) {
+  auto* ld = (__attribute__((address_space(3))) void*)l;
+  switch (j) {
+    case 0: __builtin_amdgcn_global_load_lds((const void*)g, ld, 16, 0, 0); break;
+    case 1: __builtin_amdgcn_global_load_lds((const void*)g, ld, 16, 1024, 0); break;
+    case 2: __builtin_amdgcn_global_load_lds((const void*)g, ld, 16, 2048, 0); break;
+    default: __builtin_amdgcn_global_load_lds((const void*)g, ld, 16, 3072, 0); break;
+  }
+}
+
 // Map a hardware workgroup id to a logical tile id so that each XCD (work is
 // dealt round-robin to 8 XCDs) receives one contiguous range of logical tiles;
 // neighbouring tiles then share that XCD's L2.

@@ -96,19 +96,16 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
   auto issue = [&](int kv0, int stage) {
     uint16_t* sK = smem + stage * STAGE;
     uint16_t* sV = sK + KTILE;
+    // (groups of four consecutive 1 KB blocks share one LDS base)
 #pragma unroll
     for (int i = 0; i < K_INS; ++i) {
       const int key = min(kv0 + krow[i], g.T - 1);  // keys >= T are masked below
-      __builtin_amdgcn_global_load_lds((const void*)(kb + (size_t)key * HD + koff[i]),
-                                       (__attribute__((address_space(3))) void*)(sK + (wave * K_INS + i) * 512),
-                                       16, 0, 0);
+      dma16(kb + (size_t)key * HD + koff[i] - (i & 3) * 512, sK + (wave * K_INS + (i & ~3)) * 512, i & 3);
     }
     // Tp is a multiple of 64: the whole V^T tile row lies inside the buffer
 #pragma unroll
     for (int i = 0; i < V_INS; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(vsrc[i] + kv0),
-                                       (__attribute__((address_space(3))) void*)(sV + (wave * V_INS + i) * 512),
-                                       16, 0, 0);
+      dma16(vsrc[i] + kv0 - (i & 3) * 512, sV + (wave * V_INS + (i & ~3)) * 512, i & 3);
   };
 
   bf16x8 qf[KS];

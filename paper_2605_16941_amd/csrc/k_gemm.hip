@@ -438,20 +438,18 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
     bsrc[i] = c.W + (size_t)wr * c.ldw + kbase + lkc * 8;
   }
 
+  // A wave's copies land in consecutive 1 KB blocks; groups of four share
+  // one LDS base (M0) and differ in the instruction offset.
   auto issue = [&](int kt, int stage, auto skip_tag) {
     uint16_t* sA = smem + stage * STAGE;
     uint16_t* sB = sA + AROWS * KB;
 #pragma unroll
     for (int i = 0; i < A_INS; ++i)
       if (!decltype(skip_tag)::value || alive[i])
-        __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + kt * KB),
-                                         (__attribute__((address_space(3))) void*)(sA + (wave * A_INS + i) * 512),
-                                         16, 0, 0);
+        dma16(asrc[i] + kt * KB - (i & 3) * 512, sA + (wave * A_INS + (i & ~3)) * 512, i & 3);
 #pragma unroll
     for (int i = 0; i < B_INS; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(bsrc[i] + kt * KB),
-                                       (__attribute__((address_space(3))) void*)(sB + (wave * B_INS + i) * 512),
-                                       16, 0, 0);
+      dma16(bsrc[i] + kt * KB - (i & 3) * 512, sB + (wave * B_INS + (i & ~3)) * 512, i & 3);
   };
 
   f32x16 acc[FM][FN];
