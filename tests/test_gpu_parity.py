@@ -570,6 +570,49 @@ def test_row_losses_match_oracle(P, variant):
     model.close()
 
 
+@pytest.mark.parametrize("cap_fill", [True, False])
+def test_step_cap_without_forced_draft(P, cap_fill):
+    """An unreachable draft threshold (tau1 = 1.5), no forced draft (Eq. 1
+    off) and max_steps = 3: no step drafts until the cap.  With cap fill the
+    third step drafts every remaining mask with its argmax, so each block
+    takes exactly 3 steps and the decode equals the oracle's wherever that is
+    robust; without it the decode stops with WINO_ERR_STEP_CAP and the
+    tokens untouched."""
+    cfg, w = tiny("wide", seed=2)
+    wd = to_device(w)
+    p, g, lb, B = 32, 64, 16, 2
+    model = P.WinoModel(cfg, wd, B, p + g + lb)
+    flags = P._abi.WINO_FLAG_NO_FORCE_TOP1 | (0 if cap_fill else P._abi.WINO_FLAG_NO_CAP_FILL)
+    prm_c = P.make_params(B, p, g, lb, cfg.mask_id, 1.5, 0.9, max_steps=3, flags=flags)
+    tok0 = batch_tokens(cfg, B, p, g, seed=5)
+    tok = torch.tensor(tok0, dtype=torch.int32, device="cuda")
+    bs = torch.zeros(B, dtype=torch.int32, device="cuda")
+    if not cap_fill:
+        with pytest.raises(P.WinoError) as e:
+            P.wino_decode(model.ctx, prm_c, tok, bs)
+        assert e.value.status == -5
+        torch.cuda.synchronize()
+        assert np.array_equal(tok.cpu().numpy(), tok0) and torch.all(bs == 0)
+        model.close()
+        return
+    steps, forwards = P.wino_decode(model.ctx, prm_c, tok, bs)
+    torch.cuda.synchronize()
+    assert steps == [3 * (g // lb)] * B and forwards == 3 * (g // lb)
+    got = tok.cpu().numpy()
+    assert not np.any(got[:, p:] == cfg.mask_id)
+    prm = oracle_params(prm_c, force_top1=False, cap_fill=True)
+    prov = W.ModelProvider(w, cfg, act_round=M.round_bf16)
+    compared = 0
+    for b in range(B):
+        traj, final = oracle_trajectory(prov, tok0[b], prm)
+        assert len(traj) == 3 * (g // lb)
+        if robust_trajectory(traj, p, lb, cfg.mask_id):
+            assert np.array_equal(got[b], final), f"seq {b}: decode differs from the oracle"
+            compared += 1
+    assert compared >= 1
+    model.close()
+
+
 def test_params_rejected_against_the_context(P):
     """With a live context, parameters the context cannot serve are rejected on
     the host with the documented status before any device work (batch above
