@@ -227,9 +227,11 @@ def run_other_configs(P, wi, steps, warmup, names=("mmada", "tiny")):
     return out
 
 
-def cpu_baseline(wi, cfg, weights, name):
-    """The float64 oracle on a bounded sample: one layer of one sequence plus
-    the LM head of its block rows, extrapolated to a full batched step."""
+def cpu_baseline(wi, cfg, weights, name, n_seq=4, n_layers=4):
+    """The float64 oracle on a bounded sample of the same step (about 10 s on
+    16 host threads): the first n_layers layers for n_seq of the batch's
+    sequences, plus the LM head of each one's block rows, extrapolated to
+    every layer and every sequence of one batched step."""
     import numpy as np
     import torch
     from oracle import model as M
@@ -239,26 +241,32 @@ def cpu_baseline(wi, cfg, weights, name):
     except Exception:  # pragma: no cover
         cores = os.cpu_count()
     preset, B, p, g, lb, tau1, tau2, img = CONFIGS[name]
-    lw = {k: v.cpu() for k, v in weights["layers"][0].items()}
-    tok, bs = make_state(wi, cfg, 1, p, g, lb, img)
-    ext, pos, allowed, c0 = M.extended_inputs(tok[0].numpy(), p, g, lb, int(bs[0]), cfg.mask_id)
-    emb_rows = weights["tok_emb"][torch.as_tensor(ext).cuda()].cpu()
-    w1 = {"tok_emb": emb_rows, "layers": [lw], "final_norm": weights["final_norm"].cpu(),
-          "lm_head": weights["lm_head"].cpu(), "lm_bias": weights["lm_bias"].cpu()}
-    t0 = time.perf_counter()
-    x = M.forward_residual(w1, cfg, np.arange(len(ext)), pos, allowed, n_layers=1)
-    t_layer = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    h = M.rmsnorm(x[c0:c0 + lb], M.f64(w1["final_norm"]), cfg.rms_eps)
-    M.lm_logits(w1, h)
-    t_head = time.perf_counter() - t0
-    per_seq = cfg.n_layers * t_layer + t_head
-    step_s = B * per_seq
+    n_seq, n_layers = min(n_seq, B), min(n_layers, cfg.n_layers)
+    layers = [{k: v.cpu() for k, v in weights["layers"][l].items()} for l in range(n_layers)]
+    head = {"final_norm": weights["final_norm"].cpu(), "lm_head": weights["lm_head"].cpu(),
+            "lm_bias": weights["lm_bias"].cpu()}
+    tok, bs = make_state(wi, cfg, B, p, g, lb, img)
+    t_layers = t_head = 0.0
+    T = 0
+    for s_ in range(n_seq):
+        ext, pos, allowed, c0 = M.extended_inputs(tok[s_].numpy(), p, g, lb, int(bs[s_]), cfg.mask_id)
+        T = len(ext)
+        w1 = dict(head, tok_emb=weights["tok_emb"][torch.as_tensor(ext).cuda()].cpu(), layers=layers)
+        t0 = time.perf_counter()
+        x = M.forward_residual(w1, cfg, np.arange(len(ext)), pos, allowed, n_layers=n_layers)
+        t_layers += time.perf_counter() - t0
+        t0 = time.perf_counter()
+        h = M.rmsnorm(x[c0:c0 + lb], M.f64(head["final_norm"]), cfg.rms_eps)
+        M.lm_logits(w1, h)
+        t_head += time.perf_counter() - t0
+    per_layer = t_layers / (n_seq * n_layers)
+    step_s = B * (cfg.n_layers * per_layer + t_head / n_seq)
     return {"value": round(1.0 / step_s, 6), "unit": "steps/s", "cores": int(cores), "kind": "oracle",
             "seconds_per_step": round(step_s, 2),
-            "sample": (f"float64 numpy oracle: 1 of {cfg.n_layers} layers for 1 of {B} sequences "
-                       f"(T={len(ext)}) took {t_layer:.2f}s, LM head for its {lb} block rows "
-                       f"{t_head:.2f}s; extrapolated x{cfg.n_layers} layers x{B} sequences")}
+            "sample": (f"float64 numpy oracle: {n_layers} of {cfg.n_layers} layers for {n_seq} of {B} "
+                       f"sequences (T={T}) took {t_layers:.1f}s ({per_layer:.2f}s per layer and sequence), "
+                       f"LM head of their {lb} block rows {t_head:.1f}s; extrapolated to "
+                       f"{cfg.n_layers} layers x {B} sequences")}
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_gateup_swiglu_llada8b_bs16_traffic.txt")
