@@ -306,8 +306,8 @@ def main():
                     help="also run plain device copies of known size (HBM counter calibration)")
     a = ap.parse_args()
     if a.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the WINO step is benchmarked on a single MI355X "
-              "(multi-GPU sharding is a design note, not part of this build).", file=sys.stderr)
+        print("bench.py measures one GPU only: the WINO step is benchmarked on a single MI355X; "
+              "sharding across GPUs is described, not implemented.", file=sys.stderr)
         sys.exit(2)
 
     import torch
