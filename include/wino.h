@@ -49,7 +49,7 @@ typedef enum {
   WINO_ERR_HIP = -3,         /* a HIP runtime call failed                     */
   WINO_ERR_NO_MEMORY = -4,   /* workspace allocation failed                   */
   WINO_ERR_STEP_CAP = -5,    /* a block hit its step cap with cap fill off    */
-  WINO_ERR_UNSUPPORTED = -6  /* model shape this build has no kernels for     */
+  WINO_ERR_UNSUPPORTED = -6  /* model shape the library has no kernels for    */
 } wino_status;
 
 typedef struct wino_ctx wino_ctx;
