@@ -159,10 +159,22 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
         const int pos = row_pos(g, b, t);
         uint16_t* wr = ws + lr * HD;
         const int sw = lr & (QCH - 1);
+        float cst[2 * H2];  // (cos, sin) of elements fn*32 + (lane & 31)
+        const float* tp = ro.tab + ((size_t)pos * 32 + (lane & 31)) * (2 * H2);
+        if constexpr (H2 == 2) {
+          const float4 t4 = *reinterpret_cast<const float4*>(tp);
+          cst[0] = t4.x; cst[1] = t4.y; cst[2] = t4.z; cst[3] = t4.w;
+        } else {
+#pragma unroll
+          for (int j = 0; j < H2; ++j) {
+            const float2 t2 = *reinterpret_cast<const float2*>(tp + 2 * j);
+            cst[2 * j] = t2.x; cst[2 * j + 1] = t2.y;
+          }
+        }
 #pragma unroll
         for (int fn = 0; fn < H2; ++fn) {
           const int e = fn * 32 + (lane & 31);
-          const float cs = ro.cos_t[(size_t)pos * half + e], sn = ro.sin_t[(size_t)pos * half + e];
+          const float cs = cst[2 * fn], sn = cst[2 * fn + 1];
           const float x1 = acc[fm][fn][i], x2 = acc[fm][fn + H2][i];
           const float r1 = x1 * cs - x2 * sn;  // element e
           const float r2 = x2 * cs + x1 * sn;  // element e + hd/2

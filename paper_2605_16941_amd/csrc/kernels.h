@@ -70,8 +70,10 @@ struct RopeOut {      // QKV projection + rotate-half RoPE, head-major outputs
   uint16_t* q;        // [B, H, Tp, hd]
   uint16_t* k;        // [B, H, Tp, hd]
   uint16_t* vt;       // [B, H, hd, Tp]  (value transposed: token-contiguous)
-  const float* cos_t; // [max_pos, hd/2]
-  const float* sin_t;
+  // cos and sin of the rotate-half angles, packed per lane of a 32-wide MFMA
+  // block: tab[pos][l][fn] = (cos, sin) of element e = fn*32 + l of the first
+  // half, fn < hd/64 - one 8*(hd/64)-byte load per (row, lane)
+  const float* tab;   // [max_pos][32][hd/64][2]
   int H, hd;
 };
 struct LmStatsOut {   // LM head + streaming softmax statistics per (row, N-tile)

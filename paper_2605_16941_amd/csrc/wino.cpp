@@ -32,8 +32,8 @@ constexpr int kMaxSplits = 8;
 int round64(int v) { return (v + 63) / 64 * 64; }
 
 struct Layout {
-  size_t x, h, q, k, vt, att, u, hf, hf_lo, xc, part, target, rope_cos, rope_sin, pm, ps, pb, pi, pt, pz,
-      misc, total;
+  size_t x, h, q, k, vt, att, u, hf, hf_lo, xc, part, target, rope_tab, pm, ps, pb, pi, pt, pz, misc,
+      total;
   size_t rows;  // rows the LM-head partials hold
   int max_part;
   size_t part_elems;  // split-K partial buffer (fp32 elements)
@@ -61,8 +61,7 @@ Layout make_layout(const wino_model_config& c, int max_batch, int max_seq) {
   L.part_elems = (size_t)kMaxSplits * std::min<size_t>(M, 1024) * d;
   L.part = take(L.part_elems * 4);
   L.target = take(M * 4);
-  L.rope_cos = take((size_t)max_seq * (hd / 2) * 4);
-  L.rope_sin = take((size_t)max_seq * (hd / 2) * 4);
+  L.rope_tab = take((size_t)max_seq * hd * 4);
   const size_t P = R * L.max_part;
   L.pm = take(P * 4);
   L.ps = take(P * 4);
@@ -113,8 +112,7 @@ struct wino_ctx {
   uint16_t* hf_lo() const { return at<uint16_t>(L.hf_lo); }
   float* part() const { return at<float>(L.part); }
   int32_t* target() const { return at<int32_t>(L.target); }
-  float* rope_cos() const { return at<float>(L.rope_cos); }
-  float* rope_sin() const { return at<float>(L.rope_sin); }
+  float* rope_tab() const { return at<float>(L.rope_tab); }
   int32_t* block_steps() const { return at<int32_t>(L.misc); }
   int32_t* seq_steps() const { return at<int32_t>(L.misc) + max_batch; }
   int32_t* n_masked() const { return at<int32_t>(L.misc) + 2 * max_batch; }
@@ -239,7 +237,7 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
     GemmCall qc{};
     qc.A = c->h(); qc.lda = d; qc.W = c->w_qkv[l]; qc.ldw = d;
     qc.M = M; qc.N = 3 * d; qc.K = d; qc.epi = EPI_QKV_ROPE;
-    qc.rope = RopeOut{c->q(), c->k(), c->vt(), c->rope_cos(), c->rope_sin(), H, hd};
+    qc.rope = RopeOut{c->q(), c->k(), c->vt(), c->rope_tab(), H, hd};
     qc.geom = g;
     {
       Bracket br(c, K_GEMM_QKV, st);
@@ -447,18 +445,22 @@ wino_status wino_create(const wino_model_config* cfg, const wino_weights* w, int
   }
   // zeroed workspace: padding columns of the transposed values stay finite
   if (hipMemset(c->ws, 0, c->L.total) != hipSuccess) { wino_destroy(c); return WINO_ERR_HIP; }
-  // RoPE angles pos * theta^(-2i/hd), in double precision on the host
-  const int half = cfg->head_dim / 2;
-  std::vector<float> cs((size_t)max_seq * half), sn((size_t)max_seq * half);
+  // RoPE angles pos * theta^(-2i/hd), in double precision on the host, packed
+  // as the QKV epilogue reads them: tab[pos][l][fn] = (cos, sin) of element
+  // i = fn*32 + l (the lane of a 32-wide block and its block index)
+  const int half = cfg->head_dim / 2, nblk = half / 32;
+  std::vector<float> tab((size_t)max_seq * cfg->head_dim);
   for (int pos = 0; pos < max_seq; ++pos)
-    for (int i = 0; i < half; ++i) {
-      const double inv = std::pow((double)cfg->rope_theta, -2.0 * i / cfg->head_dim);
-      const double a = pos * inv;
-      cs[(size_t)pos * half + i] = (float)std::cos(a);
-      sn[(size_t)pos * half + i] = (float)std::sin(a);
-    }
-  if (hipMemcpy(c->rope_cos(), cs.data(), cs.size() * 4, hipMemcpyHostToDevice) != hipSuccess ||
-      hipMemcpy(c->rope_sin(), sn.data(), sn.size() * 4, hipMemcpyHostToDevice) != hipSuccess) {
+    for (int l = 0; l < 32; ++l)
+      for (int fn = 0; fn < nblk; ++fn) {
+        const int i = fn * 32 + l;
+        const double inv = std::pow((double)cfg->rope_theta, -2.0 * i / cfg->head_dim);
+        const double a = pos * inv;
+        float* t = &tab[(((size_t)pos * 32 + l) * nblk + fn) * 2];
+        t[0] = (float)std::cos(a);
+        t[1] = (float)std::sin(a);
+      }
+  if (hipMemcpy(c->rope_tab(), tab.data(), tab.size() * 4, hipMemcpyHostToDevice) != hipSuccess) {
     wino_destroy(c);
     return WINO_ERR_HIP;
   }
