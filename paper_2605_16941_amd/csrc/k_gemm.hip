@@ -80,6 +80,31 @@ __device__ __forceinline__ void epi_store(const GemmCall& c, f32x16 (&acc)[FM][F
     }
 }
 
+// The fp32 epilogues through the wave's LDS region (free once the K loop has
+// drained): one 32-row block of accumulators at a time goes to LDS in the
+// MFMA layout and comes back as 16-byte row chunks, so x (residual: read, add,
+// write) or the partial buffer moves in 16-byte accesses - a quarter of the
+// memory instructions of the 4-byte accesses straight from the MFMA layout.
+// op(row, col, float4 v) gets 4 consecutive columns of one row.
+template <int FM, int FN, class Op>
+__device__ __forceinline__ void epi_rows16(f32x16 (&acc)[FM][FN], int lane, float* ws, Op op) {
+  constexpr int WTN = FN * 32, C4 = WTN / 4;
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) ws[mfma_row(i, lane) * WTN + fn * 32 + (lane & 31)] = acc[fm][fn][i];
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+    for (int it = 0; it < 32 * C4 / 64; ++it) {
+      const int idx = it * 64 + lane, r = idx / C4, c4 = idx - (idx / C4) * C4;
+      op(fm * 32 + r, c4 * 4, *reinterpret_cast<const float4*>(ws + r * WTN + c4 * 4));
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  }
+}
+
 // K-slice `split` of a tile above split_row0: fp32 partial
 // part[split][m - split_row0][n] (row stride N), summed into x later.
 template <int FM, int FN>
@@ -606,8 +631,31 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
 
   const int rowb = m0 + wm * WTM, colb = n0 + wn * WTN;
   if constexpr (EPI == EPI_RESIDUAL) {
-    if (!(ksplit && tail)) epi_residual<FM, FN>(c, acc, rowb, colb, lane);
-    else epi_partial<FM, FN>(c, acc, rowb, colb, lane, split);
+    // a wave's LDS region holds one 32-row fp32 block of its tile
+    constexpr bool STAGED = NW * 32 * WTN * 2 <= NST * STAGE;
+    if constexpr (STAGED) {
+      float* ws = reinterpret_cast<float*>(smem + wave * (32 * WTN * 2));
+      if (!(ksplit && tail)) {
+        epi_rows16<FM, FN>(acc, lane, ws, [&](int lr, int lc, float4 v) {
+          const int row = rowb + lr;
+          if (row >= c.M) return;
+          float4* dst = reinterpret_cast<float4*>(c.outf + (size_t)row * c.ldc + colb + lc);
+          float4 x = *dst;
+          x.x += v.x; x.y += v.y; x.z += v.z; x.w += v.w;
+          *dst = x;
+        });
+      } else {
+        const size_t mt = (size_t)(c.M - c.split_row0);
+        epi_rows16<FM, FN>(acc, lane, ws, [&](int lr, int lc, float4 v) {
+          const int row = rowb + lr;
+          if (row >= c.M) return;
+          *reinterpret_cast<float4*>(c.part + (split * mt + (row - c.split_row0)) * c.N + colb + lc) = v;
+        });
+      }
+    } else {
+      if (!(ksplit && tail)) epi_residual<FM, FN>(c, acc, rowb, colb, lane);
+      else epi_partial<FM, FN>(c, acc, rowb, colb, lane, split);
+    }
   }
   else if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_LOGITS) epi_store<FM, FN>(c, acc, rowb, colb, lane);
   else if constexpr (EPI == EPI_SWIGLU) epi_swiglu<FM, FN>(c, acc, rowb, colb, lane);
