@@ -168,7 +168,8 @@ def run_epilogue(P, wi, n_calls=20, n_buf=4):
     """Standalone WINO epilogue on given bf16 logits [8, 64, 126464] (the
     decision of Eq. 2-4 read from materialised logits), timed with HIP events
     over n_calls calls rotating n_buf logit buffers (more bytes than the 256 MB
-    Infinity Cache holds), each call on a fresh copy of the block state."""
+    Infinity Cache holds), each call on a fresh copy of the block state, all
+    queued behind a spin kernel so the host's per-call overhead is not timed."""
     import torch
     B, lb, V, mask = 8, 32, 126464, 126463
     bufs, curs = [], []
@@ -184,6 +185,9 @@ def run_epilogue(P, wi, n_calls=20, n_buf=4):
     for i in range(2):
         P.wino_epilogue(prm, V, bufs[i % n_buf], curs[i % n_buf].clone(), bitmap, workspace=ws)
     torch.cuda.synchronize()
+    # a spin kernel first, so every call below is queued before the GPU gets to
+    # them: the events then time the device work, not the host's call overhead
+    torch.cuda._sleep(20_000_000)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for i in range(n_calls):
