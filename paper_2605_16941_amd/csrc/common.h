@@ -63,6 +63,12 @@ __device__ __forceinline__ void dma16(const uint16_t* g, uint16_t* l, int j) {
   }
 }
 
+// Raw buffer resources (stride 0; the range is in bytes): word 3 for the gfx9
+// family, and a vector offset beyond any range used here, whose access the
+// range check drops (loads return 0).
+constexpr int kBufferDword3 = 0x00020000;
+constexpr int kBufferOffNone = INT32_MIN;
+
 // Map a hardware workgroup id to a logical tile id so that each XCD (work is
 // dealt round-robin to 8 XCDs) receives one contiguous range of logical tiles;
 // neighbouring tiles then share that XCD's L2.

@@ -123,25 +123,71 @@ __device__ __forceinline__ void epi_partial(const GemmCall& c, f32x16 (&acc)[FM]
     }
 }
 
+// out = silu(gate) * up = g u / (1 + 2^(-g log2 e)), with the hardware exp2
+// and reciprocal (about 1 ulp of fp32 each, far below the bf16 rounding that
+// follows; an IEEE divide is ~10 VALU instructions per element, and the
+// epilogue runs while the matrix cores of the CU idle).  Stores are buffer
+// stores: the row offset of each accumulator register is wave-uniform and
+// goes in a scalar register, the lane's column in the vector offset.  In a
+// tile that crosses the last row, rows past it get an offset beyond the
+// buffer range, which drops their stores.
 template <int FM, int FN>
 __device__ __forceinline__ void epi_swiglu(const GemmCall& c, f32x16 (&acc)[FM][FN], int rowb,
                                            int colb, int lane) {
-  constexpr int H2 = FN / 2;
-  const int fb = colb / 2 + (lane & 31);
+  constexpr int H2 = FN / 2, WTM = FM * 32;
+  // wave-uniform: the resource and the row offsets live in scalar registers
+  rowb = __builtin_amdgcn_readfirstlane(rowb);
+  colb = __builtin_amdgcn_readfirstlane(colb);
+  if (rowb >= c.M) return;
+  const int nrows = min(c.M - rowb, WTM), ld2 = c.ldc * 2;
+  const auto rs = __builtin_amdgcn_make_buffer_rsrc(c.outh + (size_t)rowb * c.ldc + colb / 2, (short)0,
+                                                    nrows * ld2, kBufferDword3);
+  const int lrow = 4 * (lane >> 5);
+  const int voff = lrow * ld2 + (lane & 31) * 2;
+  auto body = [&](auto full) {
 #pragma unroll
-  for (int fm = 0; fm < FM; ++fm)
+    for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int row = rowb + fm * 32 + mfma_row(i, lane);
-      if (row >= c.M) continue;
-      uint16_t* dst = c.outh + (size_t)row * c.ldc + fb;
+      for (int i = 0; i < 16; ++i) {
+        const int srow = fm * 32 + 8 * (i >> 2) + (i & 3);
+        int vo = voff;
+        if constexpr (!decltype(full)::value) vo = srow + lrow < nrows ? voff : kBufferOffNone;
 #pragma unroll
-      for (int fn = 0; fn < H2; ++fn) {
-        const float g = acc[fm][fn][i], u = acc[fm][fn + H2][i];
-        dst[fn * 32] = f2bf(g / (1.f + __expf(-g)) * u);
+        for (int fn = 0; fn < H2; ++fn) {
+          const float g = acc[fm][fn][i], u = acc[fm][fn + H2][i];
+          const float sg = __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(g * -1.44269504088896341f));
+          __builtin_amdgcn_raw_buffer_store_b16(f2bf(g * u * sg), rs, vo + fn * 64, srow * ld2, 0);
+        }
       }
-    }
+  };
+  if (nrows == WTM) body(std::true_type{});
+  else body(std::false_type{});
 }
+
+// Sequence b and position t of row rowb + lr of a wave's tile (rows are
+// sequence-major, T per sequence).  TWO: the sequences are at least as long
+// as the tile, so it spans at most two of them - one division per wave and a
+// compare per row instead of a division per row.
+template <bool TWO>
+struct TileRows {
+  int b0, t0, T;
+  __device__ __forceinline__ TileRows(int rowb, int T_) : T(T_) {
+    b0 = rowb / T;
+    t0 = rowb - b0 * T;
+  }
+  __device__ __forceinline__ void at(int lr, int& b, int& t) const {
+    if constexpr (TWO) {
+      t = t0 + lr;
+      const bool nx = t >= T;
+      t = nx ? t - T : t;
+      b = b0 + (int)nx;
+    } else {
+      const int r = b0 * T + t0 + lr;
+      b = r / T;
+      t = r - b * T;
+    }
+  }
+};
 
 // Wave columns = one head (WTN == hd): lane holds columns e and e + hd/2 of
 // the rotate-half pair in fragments fn and fn + FN/2.  The wave's rotated q/k
@@ -151,7 +197,7 @@ __device__ __forceinline__ void epi_swiglu(const GemmCall& c, f32x16 (&acc)[FM][
 // MFMA layout would scatter 2-byte writes over hd rows of the transposed
 // buffer.  16-byte chunks are XOR-swizzled by the row index, so the
 // half-waves' writes (4 rows apart) land in distinct banks.
-template <int FM, int FN>
+template <int FM, int FN, bool TWO>
 __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM][FN], int rowb,
                                              int colb, int lane, uint16_t* ws) {
   constexpr int H2 = FN / 2;
@@ -172,16 +218,25 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
   const int d = ro.H * HD;
   const int which = colb / d;               // 0 q, 1 k, 2 v
   const int head = (colb - which * d) / HD;
+  if (rowb >= c.M) return;  // a wave wholly past the last row
+  const TileRows<TWO> tr(rowb, g.T);
   if (which < 2) {
+    // block starts of the wave's first two sequences (the second clamped to
+    // the batch: rows past the last compute a valid but unused position)
+    const int cs0 = cur_start(g, tr.b0), cs1 = cur_start(g, min(tr.b0 + 1, g.B - 1));
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
+        // rows past the last are staged too (their q/k never leave LDS)
         const int lr = fm * 32 + mfma_row(i, lane);
-        const int row = rowb + lr;
-        if (row >= c.M) continue;
-        const int b = row / g.T, t = row - b * g.T;
-        const int pos = row_pos(g, b, t);
+        int b, t;
+        tr.at(lr, b, t);
+        int pos = t;
+        if (t >= g.S) {
+          if constexpr (TWO) pos = (b == tr.b0 ? cs0 : cs1) + (t - g.S);
+          else pos = cur_start(g, min(b, g.B - 1)) + (t - g.S);
+        }
         uint16_t* wr = ws + lr * HD;
         const int sw = lr & (QCH - 1);
         float cst[2 * H2];  // (cos, sin) of elements fn*32 + (lane & 31)
@@ -201,8 +256,10 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
           const int e = fn * 32 + (lane & 31);
           const float cs = cst[2 * fn], sn = cst[2 * fn + 1];
           const float x1 = acc[fm][fn][i], x2 = acc[fm][fn + H2][i];
-          const float r1 = x1 * cs - x2 * sn;  // element e
-          const float r2 = x2 * cs + x1 * sn;  // element e + hd/2
+          // explicit FMAs: the rounding does not depend on how the compiler
+          // contracts the products
+          const float r1 = fmaf(x1, cs, -(x2 * sn));  // element e
+          const float r2 = fmaf(x2, cs, x1 * sn);     // element e + hd/2
           // lane pairs trade one value: the even lane stores elements e, e+1,
           // the odd lane elements e+hd/2-1, e+hd/2 (one 4-byte write each)
           const bool odd = lane & 1;
@@ -218,9 +275,9 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
 #pragma unroll
     for (int it = 0; it < WTM / RPI; ++it) {
       const int lr = it * RPI + lane / QCH, ch = lane & (QCH - 1);
-      const int row = rowb + lr;
-      if (row >= c.M) continue;
-      const int b = row / g.T, t = row - b * g.T;
+      if (rowb + lr >= c.M) continue;
+      int b, t;
+      tr.at(lr, b, t);
       const size_t bh = (size_t)b * ro.H + head;
       const uint4 v = *reinterpret_cast<const uint4*>(ws + lr * HD + ((ch ^ (lr & (QCH - 1))) << 3));
       *reinterpret_cast<uint4*>(base + (bh * g.Tp + t) * HD + ch * 8) = v;
@@ -254,7 +311,8 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
       if (m & 1) v = make_uint4(v.z, v.w, v.x, v.y);
       const int r0 = rowb + ch * 8;
       if (r0 >= c.M) continue;
-      const int b = r0 / g.T, t0 = r0 - b * g.T;
+      int b, t0;
+      tr.at(ch * 8, b, t0);
       if (r0 + 7 < c.M && t0 + 7 < g.T && (t0 & 7) == 0) {
         const size_t bh = (size_t)b * ro.H + head;
         *reinterpret_cast<uint4*>(ro.vt + (bh * HD + e) * g.Tp + t0) = v;
@@ -662,7 +720,8 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
   else if constexpr (EPI == EPI_QKV_ROPE) {
     // each wave stages its WTM x WTN tile in its own LDS region
     static_assert(BM * BN <= NST * STAGE, "QKV staging fits the pipeline LDS");
-    epi_qkv_rope<FM, FN>(c, acc, rowb, colb, lane, smem + wave * (WTM * WTN));
+    if (c.geom.T >= WTM) epi_qkv_rope<FM, FN, true>(c, acc, rowb, colb, lane, smem + wave * (WTM * WTN));
+    else epi_qkv_rope<FM, FN, false>(c, acc, rowb, colb, lane, smem + wave * (WTM * WTN));
   }
   else epi_lmstats<BM, WM, WN, FM, FN>(c, acc, m0, tn, rowb, colb, lane, wm, wn, smem);
 }
