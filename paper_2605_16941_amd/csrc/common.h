@@ -48,6 +48,18 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Reductions over the lane pair (l, l ^ 32): v_permlane32_swap exchanges the
+// two 32-lane halves between registers, where a shuffle goes through the LDS
+// crossbar (ds_bpermute) and its latency.  Both lanes get the same value.
+__device__ __forceinline__ float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // LDS-DMA of 16 bytes per lane (global_load_lds_dwordx4) into the 1 KB block
 // at l + j KB (j = 0..3): the LDS base goes to M0 and j KB into the
 // instruction's offset, which applies to the global address as well, so g

@@ -191,7 +191,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
     for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
       for (int i = 0; i < 16; ++i) tmax = fmaxf(tmax, s[kb2][i]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    tmax = max_xor32(tmax);
     // Reference max mrun in raw score units; probabilities exp2(s*c - m*c)
     // with c = log2(e)/sqrt(hd): one FMA per score.  The reference moves
     // (and O, l are rescaled) only when a score exceeds it by more than
@@ -200,7 +200,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
     const bool resc = tmax > mrun + rescale_gap;
     if (__any(resc)) {
       const float mnew = resc ? tmax : mrun;
-      const float alpha = exp2f((mrun - mnew) * scale_log2);
+      const float alpha = __builtin_amdgcn_exp2f((mrun - mnew) * scale_log2);
       lrun *= alpha;
       mrun = mnew;
 #pragma unroll
@@ -209,12 +209,15 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
         for (int i = 0; i < 16; ++i) oacc[fe][i] *= alpha;
     }
     const float mc = mrun == kNegBig ? 0.f : mrun * scale_log2;
+    // the hardware exp2 (v_exp_f32): results below 2^-126 flush to zero,
+    // which next to a running sum of at least one changes nothing; the
+    // library exp2f adds five instructions per score to keep them
     float psum = 0.f;
 #pragma unroll
     for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float p = exp2f(fmaf(s[kb2][i], scale_log2, -mc));
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[kb2][i], scale_log2, -mc));
         s[kb2][i] = p;
         psum += p;
       }
@@ -240,7 +243,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
     }
   }
 
-  lrun += __shfl_xor(lrun, 32, 64);
+  lrun = sum_xor32(lrun);
   if (qvalid) {
     const float inv = 1.f / lrun;
     const size_t orow = CQ ? (size_t)b * NQ + ci : (size_t)b * g.T + myq;

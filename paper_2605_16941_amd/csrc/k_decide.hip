@@ -312,11 +312,13 @@ __global__ __launch_bounds__(256) void epi_stats_kernel(const uint16_t* __restri
       }
   }
   const float mc = m * kLog2e;
+  // hardware exp2: terms below 2^-126 flush to zero, nothing next to the
+  // max's term of one
   float se = 0.f;
 #pragma unroll
   for (int it = 0; it < IT; ++it)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) se += exp2f(fmaf(elem(it, e), kLog2e, -mc));
+    for (int e = 0; e < 8; ++e) se += __builtin_amdgcn_exp2f(fmaf(elem(it, e), kLog2e, -mc));
   se = wave_sum(se);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) bi = min(bi, __shfl_xor(bi, o, 64));
