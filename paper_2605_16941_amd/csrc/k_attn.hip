@@ -99,8 +99,10 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
     // (groups of four consecutive 1 KB blocks share one LDS base)
 #pragma unroll
     for (int i = 0; i < K_INS; ++i) {
-      const int key = min(kv0 + krow[i], g.T - 1);  // keys >= T are masked below
-      dma16(kb + (size_t)key * HD + koff[i] - (i & 3) * 512, sK + (wave * K_INS + (i & ~3)) * 512, i & 3);
+      // rows [T, Tp) of the padded buffer (zero from creation, or finite
+      // rows of an earlier call) are read like the V^T padding and masked
+      dma16(kb + (size_t)(kv0 + krow[i]) * HD + koff[i] - (i & 3) * 512,
+            sK + (wave * K_INS + (i & ~3)) * 512, i & 3);
     }
     // Tp is a multiple of 64: the whole V^T tile row lies inside the buffer
 #pragma unroll
