@@ -351,7 +351,8 @@ def test_teacher_forced_steps(P, variant, tau1, tau2):
 # ---------------------------------------------------------------- free-running decode
 @pytest.mark.parametrize("variant,tau1,tau2,lb", [("wide", 0.7, 0.9, 16), ("literal", 0.7, 0.9, 16),
                                                   ("wide", 0.6, 0.9, 64), ("wide", 0.8, 0.95, 8),
-                                                  ("wide", 0.9, 0.0, 16)])
+                                                  ("wide", 0.9, 0.0, 16), ("wide", 0.7, 0.9, 1),
+                                                  ("wide", 1.0, 0.0, 16)])
 def test_decode_matches_oracle(P, variant, tau1, tau2, lb):
     cfg, w = tiny(variant, seed=2)
     wd = to_device(w)
@@ -525,6 +526,36 @@ def test_baseline_decoders_match_oracle(P, m):
     got = tok.cpu().numpy()
     assert forwards == (g // lb) * -(-lb // m) and all(s_ == forwards for s_ in steps)
     assert not np.any(got[:, p:] == cfg.mask_id) and np.array_equal(got[:, :p], tok0[:, :p])
+    model.close()
+
+
+@pytest.mark.parametrize("tau1,m", [(1.0, 1), (-1.0, 16)])
+def test_threshold_special_cases_equal_baselines(P, tau1, m):
+    """Sec. 5 special cases on the same kernels: with tau2 = 0 nothing is
+    re-masked; tau1 >= 1 then drafts only the forced top-1 position (Eq. 2 can
+    never exceed 1), which is Eq. 1 greedy decoding, one token per step; tau1 < 0
+    drafts every masked position at once, one step per block.  Both must equal
+    the fixed-schedule baselines (tokens_per_step 1 and L_b) bit for bit: the
+    same forward (no shadow block in either) and the same confidence ranking,
+    ties to the lowest position."""
+    cfg, w = tiny("wide", seed=4)
+    wd = to_device(w)
+    p, g, lb, B = 32, 64, 16, 2
+    model = P.WinoModel(cfg, wd, B, p + g + lb)
+    tok0 = batch_tokens(cfg, B, p, g, seed=12)
+    outs = []
+    for prm_c in (P.make_params(B, p, g, lb, cfg.mask_id, tau1, 0.0),
+                  P.make_params(B, p, g, lb, cfg.mask_id, tokens_per_step=m)):
+        tok = torch.tensor(tok0, dtype=torch.int32, device="cuda")
+        bs = torch.zeros(B, dtype=torch.int32, device="cuda")
+        steps, forwards = P.wino_decode(model.ctx, prm_c, tok, bs)
+        torch.cuda.synchronize()
+        outs.append((tok.cpu().numpy(), list(steps), forwards))
+    (wt, ws, wf), (bt, bsteps, bf) = outs
+    assert wf == bf == (g // lb) * -(-lb // m)
+    assert ws == bsteps == [wf] * B
+    assert not np.any(wt[:, p:] == cfg.mask_id) and np.array_equal(wt[:, :p], tok0[:, :p])
+    assert np.array_equal(wt, bt)
     model.close()
 
 
