@@ -220,7 +220,41 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
   const int head = (colb - which * d) / HD;
   if (rowb >= c.M) return;  // a wave wholly past the last row
   const TileRows<TWO> tr(rowb, g.T);
-  if (which < 2) {
+  // A wave whose rows are all normal rows of one sequence has position = t:
+  // its table rows follow one base pointer at constant offsets, and each lane
+  // writes its two rotated values (elements e and e + 64) as 16-bit stores.
+  // The staged layout is the general path's: element e of row r in 16-byte
+  // chunk (e >> 3) ^ (r & 15).  With r = lrc + 4*g (lrc the row's constant
+  // part, g = lane / 32) that chunk is c8 | ((fn ^ g) << 2) | (q ^ (i & 3)),
+  // q = (lane & 31) / 8, c8 = bit 3 of lrc, and element e + 64 flips bit 3:
+  // a per-lane base and a compile-time offset for every store.
+  bool plain = false;
+  if constexpr (TWO && HD == 128) plain = which < 2 && tr.t0 + WTM <= g.S;
+  if (plain) {
+    const int g4 = lane >> 5, q8 = (lane & 31) >> 3;
+    const float* tb = ro.tab + ((size_t)(tr.t0 + 4 * g4) * 32 + (lane & 31)) * 4;
+    uint16_t* wl = ws + 4 * g4 * HD + (lane & 7);
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int i3 = i & 3, c8 = 8 * ((i >> 2) & 1);
+        const int lrc = fm * 32 + 8 * (i >> 2) + i3;
+        const float4 t4 = *reinterpret_cast<const float4*>(tb + (size_t)lrc * 128);
+        const float cst[4] = {t4.x, t4.y, t4.z, t4.w};
+#pragma unroll
+        for (int fn = 0; fn < 2; ++fn) {
+          const float cs = cst[2 * fn], sn = cst[2 * fn + 1];
+          const float x1 = acc[fm][fn][i], x2 = acc[fm][fn + 2][i];
+          const float r1 = fmaf(x1, cs, -(x2 * sn));  // element e
+          const float r2 = fmaf(x2, cs, x1 * sn);     // element e + hd/2
+          const uint32_t pk = pack2bf(r1, r2);
+          uint16_t* row = wl + lrc * HD + (((((fn ^ g4) << 2) | (q8 ^ i3))) << 3);
+          row[c8 << 3] = (uint16_t)pk;
+          row[(c8 ^ 8) << 3] = (uint16_t)(pk >> 16);
+        }
+      }
+  } else if (which < 2) {
     // block starts of the wave's first two sequences (the second clamped to
     // the batch: rows past the last compute a valid but unused position)
     const int cs0 = cur_start(g, tr.b0), cs1 = cur_start(g, min(tr.b0 + 1, g.B - 1));
@@ -269,6 +303,8 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
           *reinterpret_cast<uint32_t*>(wr + (((ee >> 3) ^ sw) << 3) + (ee & 7)) = pk;
         }
       }
+  }
+  if (which < 2) {
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     uint16_t* base = which == 0 ? ro.q : ro.k;
     constexpr int RPI = 64 / QCH;  // rows per pass
