@@ -75,6 +75,17 @@ __device__ __forceinline__ void dma16(const uint16_t* g, uint16_t* l, int j) {
   }
 }
 
+// A pointer known to be the same in every lane, moved to scalar registers
+// (values computed on the vector unit, e.g. from a division, otherwise make
+// the compiler loop over lanes to build a buffer resource from them).
+template <class T>
+__device__ __forceinline__ T* uniform_ptr(T* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<T*>(((uint64_t)hi << 32) | lo);
+}
+
 // Raw buffer resources (stride 0; the range is in bytes): word 3 for the gfx9
 // family, and a vector offset beyond any range used here, whose access the
 // range check drops (loads return 0).

@@ -214,12 +214,18 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
   static_assert((HD * VCH) % 64 == 0, "v^T chunking");
   const RopeOut& ro = c.rope;
   const StepGeom& g = c.geom;
+  // wave-uniform: store bases and row offsets live in scalar registers
+  rowb = __builtin_amdgcn_readfirstlane(rowb);
+  colb = __builtin_amdgcn_readfirstlane(colb);
   const int half = HD / 2;
   const int d = ro.H * HD;
   const int which = colb / d;               // 0 q, 1 k, 2 v
   const int head = (colb - which * d) / HD;
   if (rowb >= c.M) return;  // a wave wholly past the last row
   const TileRows<TWO> tr(rowb, g.T);
+  // the wave's first sequence and position, marked uniform (the division
+  // runs on the vector unit) so the store bases below stay scalar
+  const int b0u = __builtin_amdgcn_readfirstlane(tr.b0), t0u = __builtin_amdgcn_readfirstlane(tr.t0);
   // A wave whose rows are all normal rows of one sequence has position = t:
   // its table rows follow one base pointer at constant offsets, and each lane
   // writes its two rotated values (elements e and e + 64) as 16-bit stores.
@@ -232,7 +238,7 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
   if constexpr (TWO && HD == 128) plain = which < 2 && tr.t0 + WTM <= g.S;
   if (plain) {
     const int g4 = lane >> 5, q8 = (lane & 31) >> 3;
-    const float* tb = ro.tab + ((size_t)(tr.t0 + 4 * g4) * 32 + (lane & 31)) * 4;
+    const float* tb = ro.tab + ((size_t)(t0u + 4 * g4) * 32 + (lane & 31)) * 4;
     uint16_t* wl = ws + 4 * g4 * HD + (lane & 7);
 #pragma unroll
     for (int fm = 0; fm < FM; ++fm)
@@ -308,6 +314,24 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     uint16_t* base = which == 0 ? ro.q : ro.k;
     constexpr int RPI = 64 / QCH;  // rows per pass
+    if (tr.t0 + WTM <= g.T && rowb + WTM <= c.M) {
+      // the wave's rows are one contiguous block of one sequence: 16-byte
+      // stores from a wave-uniform base at per-lane plus constant offsets
+      // (no per-row position, address or bounds arithmetic).  Not buffer
+      // stores with the row offset in a scalar register: after such a 16-byte
+      // store the compiler let the next instruction overwrite its data
+      // register with no wait state, and one dword of it was lost.
+      const size_t bh = (size_t)b0u * ro.H + head;
+      uint16_t* dst = uniform_ptr(base + (bh * g.Tp + t0u) * HD);
+      const int lrl = lane / QCH, ch = lane & (QCH - 1);
+      uint16_t* dl = dst + lrl * HD + ch * 8;
+#pragma unroll
+      for (int it = 0; it < WTM / RPI; ++it) {
+        const int lr = it * RPI + lrl;
+        const uint4 v = *reinterpret_cast<const uint4*>(ws + lr * HD + ((ch ^ (lr & (QCH - 1))) << 3));
+        *reinterpret_cast<uint4*>(dl + it * RPI * HD) = v;
+      }
+    } else {
 #pragma unroll
     for (int it = 0; it < WTM / RPI; ++it) {
       const int lr = it * RPI + lane / QCH, ch = lane & (QCH - 1);
@@ -317,6 +341,7 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
       const size_t bh = (size_t)b * ro.H + head;
       const uint4 v = *reinterpret_cast<const uint4*>(ws + lr * HD + ((ch ^ (lr & (QCH - 1))) << 3));
       *reinterpret_cast<uint4*>(base + (bh * g.Tp + t) * HD + ch * 8) = v;
+    }
     }
   } else {
     // v^T staging: LDS row e holds the WTM positions of this wave; lane writes
@@ -338,6 +363,24 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
         }
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    if (tr.t0 + WTM <= g.T && rowb + WTM <= c.M && (tr.t0 & 7) == 0) {
+      // one sequence, no row past M, 16-byte aligned runs: the head's v^T
+      // rows from a wave-uniform base (position t0) at per-lane offsets
+      constexpr int EPP = 64 / VCH;  // v^T rows per pass
+      const size_t bh = (size_t)b0u * ro.H + head;
+      uint16_t* dst = uniform_ptr(ro.vt + bh * HD * g.Tp + t0u);
+      const int el = lane / VCH, ch = lane % VCH;
+      uint16_t* dl = dst + (size_t)el * g.Tp + ch * 8;
+#pragma unroll
+      for (int it = 0; it < HD * VCH / 64; ++it) {
+        const int e = it * EPP + el;
+        const int m = (e >> 1) & SMASK;
+        uint4 v = *reinterpret_cast<const uint4*>(ws + e * WTM + ((ch ^ (m >> 1)) << 3));
+        if (m & 1) v = make_uint4(v.z, v.w, v.x, v.y);
+        *reinterpret_cast<uint4*>(dl + (size_t)it * EPP * g.Tp) = v;
+      }
+      return;
+    }
 #pragma unroll
     for (int it = 0; it < HD * VCH / 64; ++it) {
       const int idx = it * 64 + lane;
