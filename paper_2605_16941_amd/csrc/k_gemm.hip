@@ -105,6 +105,40 @@ __device__ __forceinline__ void epi_rows16(f32x16 (&acc)[FM][FN], int lane, floa
   }
 }
 
+// x += acc for a wave tile whose rows all lie below M, through the wave's LDS
+// region like epi_rows16: a 32-row block's x loads all go out before its
+// adds and stores (in program order, so the compiler need not prove the
+// runtime-strided stores and loads apart, and one memory round trip covers
+// the block instead of one per 16-byte chunk).  xb: the tile's x at
+// (rowb, colb), the same in every lane.
+template <int FM, int FN>
+__device__ __forceinline__ void epi_residual_full(f32x16 (&acc)[FM][FN], int lane, float* ws, float* xb,
+                                                  int ldc) {
+  constexpr int WTN = FN * 32, C4 = WTN / 4, IT = 32 * C4 / 64;
+  const int r0 = lane / C4, c4 = lane % C4;
+  float* xl = xb + (size_t)r0 * ldc + c4 * 4;
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+    float4 xv[IT];
+#pragma unroll
+    for (int it = 0; it < IT; ++it)
+      xv[it] = *reinterpret_cast<const float4*>(xl + (size_t)(fm * 32 + it * (64 / C4)) * ldc);
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) ws[mfma_row(i, lane) * WTN + fn * 32 + (lane & 31)] = acc[fm][fn][i];
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const float4 v = *reinterpret_cast<const float4*>(ws + (it * (64 / C4) + r0) * WTN + c4 * 4);
+      float4 x = xv[it];
+      x.x += v.x; x.y += v.y; x.z += v.z; x.w += v.w;
+      *reinterpret_cast<float4*>(xl + (size_t)(fm * 32 + it * (64 / C4)) * ldc) = x;
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  }
+}
+
 // K-slice `split` of a tile above split_row0: fp32 partial
 // part[split][m - split_row0][n] (row stride N), summed into x later.
 template <int FM, int FN>
@@ -772,7 +806,13 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
     constexpr bool STAGED = NW * 32 * WTN * 2 <= NST * STAGE;
     if constexpr (STAGED) {
       float* ws = reinterpret_cast<float*>(smem + wave * (32 * WTN * 2));
-      if (!(ksplit && tail)) {
+      // (the batched x loads need 64 registers beside the accumulators: only
+      // for wave tiles of at most 8 MFMA blocks)
+      if (FM * FN <= 8 && !(ksplit && tail) && rowb + WTM <= c.M) {
+        const int rbu = __builtin_amdgcn_readfirstlane(rowb), cbu = __builtin_amdgcn_readfirstlane(colb);
+        if constexpr (FM * FN <= 8)
+          epi_residual_full<FM, FN>(acc, lane, ws, c.outf + (size_t)rbu * c.ldc + cbu, c.ldc);
+      } else if (!(ksplit && tail)) {
         epi_rows16<FM, FN>(acc, lane, ws, [&](int lr, int lc, float4 v) {
           const int row = rowb + lr;
           if (row >= c.M) return;
