@@ -561,11 +561,15 @@ __device__ __forceinline__ int lds_swz(int r) {
 }
 
 // OCC workgroups per CU: the launch bound asks for OCC * waves / 4 waves per
-// SIMD, which caps the registers per wave accordingly.
-template <int BM, int BN, int WM, int WN, int EPI, int KB, int NST, int OCC>
+// SIMD, which caps the registers per wave accordingly.  XW > 0 gives the W
+// tiles XW more LDS stages than the two of A, so W copies have 1 + XW K
+// steps to land instead of one (for weights that few row tiles share, whose
+// copies mostly miss L2).
+template <int BM, int BN, int WM, int WN, int EPI, int KB, int NST, int OCC, int XW>
 __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_kernel(const GemmCall c) {
   static_assert(KB == 32 || KB == 64, "K step");
   static_assert(NST >= 2, "pipeline stages");
+  static_assert(XW == 0 || (XW <= 2 && NST == 2), "extra W stages beside two A stages");
   constexpr int NW = WM * WN;
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int FM = WTM / 32, FN = WTN / 32;
@@ -580,9 +584,11 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
   constexpr int INS = A_INS + B_INS;
   static_assert(A_INS * RPI * NW == AROWS && B_INS * RPI * NW == BN, "loader split");
   static_assert(FM >= 1 && FN >= 1, "wave tile");
-  constexpr int STAGE = (AROWS + BN) * KB;  // bf16 elements per pipeline stage
+  constexpr int NSB = NST + XW;  // W stages
+  constexpr int A_STAGE = AROWS * KB, B_STAGE = BN * KB;  // bf16 elements per stage
+  constexpr int LDS_ELEMS = NST * A_STAGE + NSB * B_STAGE;  // A stages, then W stages
 
-  __shared__ __attribute__((aligned(1024))) uint16_t smem[NST * STAGE];
+  __shared__ __attribute__((aligned(1024))) uint16_t smem[LDS_ELEMS];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave - (wave / WN) * WN;
@@ -623,7 +629,7 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
   // past M and the copies of A rows past M (they feed only output rows past
   // M); with two stages every later wait is for all of a wave's copies, so
   // only the first wait changes.
-  constexpr bool CAN_SKIP = NST == 2 && !SPLIT && NW == 8;
+  constexpr bool CAN_SKIP = NST == 2 && !SPLIT && NW == 8;  // (W copies are never skipped)
   bool alive[A_INS];
   const uint16_t* asrc[A_INS];
 #pragma unroll
@@ -648,13 +654,17 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
 
   // A wave's copies land in consecutive 1 KB blocks; groups of four share
   // one LDS base (M0) and differ in the instruction offset.
-  auto issue = [&](int kt, int stage, auto skip_tag) {
-    uint16_t* sA = smem + stage * STAGE;
-    uint16_t* sB = sA + AROWS * KB;
+  auto stage_a = [&](int s) { return smem + s * A_STAGE; };
+  auto stage_b = [&](int s) { return smem + NST * A_STAGE + s * B_STAGE; };
+  auto issue_a = [&](int kt, int stage, auto skip_tag) {
+    uint16_t* sA = stage_a(stage);
 #pragma unroll
     for (int i = 0; i < A_INS; ++i)
       if (!decltype(skip_tag)::value || alive[i])
         dma16(asrc[i] + kt * KB - (i & 3) * 512, sA + (wave * A_INS + (i & ~3)) * 512, i & 3);
+  };
+  auto issue_b = [&](int kt, int stage) {
+    uint16_t* sB = stage_b(stage);
 #pragma unroll
     for (int i = 0; i < B_INS; ++i)
       dma16(bsrc[i] + kt * KB - (i & 3) * 512, sB + (wave * B_INS + (i & ~3)) * 512, i & 3);
@@ -697,9 +707,8 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
   constexpr int NR = FMV ? FMV + FN + (SPLIT ? FMV : 0) : 0;  // LDS fragment reads per 16-deep step
   constexpr int NM = FMV * FN * (SPLIT ? 2 : 1);              // MFMAs per step
   constexpr int RI = NR < NM ? NR : NM;                       // reads interleaved with MFMAs
-  auto load_frags = [&](const uint16_t* sA, int ks, int buf) {
+  auto load_frags = [&](const uint16_t* sA, const uint16_t* sB, int ks, int buf) {
     if constexpr (FMV > 0) {
-    const uint16_t* sB = sA + AROWS * KB;
     const int kc = ks * 2 + (lane >> 5);
 #pragma unroll
     for (int fm = 0; fm < FMV; ++fm)
@@ -730,10 +739,10 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
     }
   };
   // steps 0..KS-2 of a tile: the reads of step ks+1 go between the MFMAs of ks
-  auto inner_steps = [&](const uint16_t* sA) {
+  auto inner_steps = [&](const uint16_t* sA, const uint16_t* sB) {
 #pragma unroll
     for (int ks = 0; ks + 1 < KS; ++ks) {
-      load_frags(sA, ks + 1, (ks + 1) & 1);
+      load_frags(sA, sB, ks + 1, (ks + 1) & 1);
       mfmas(ks & 1);
     }
     if constexpr (NR > 0) {
@@ -758,28 +767,49 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
   // issues the first fragment reads of tile t+1, and only then (5) runs the
   // last MFMAs of tile t, which cover the latency of those reads.  Tiles past
   // the end are refetches of the last one, which keeps the wait counts fixed.
+  // With XW extra W stages the crossing issues the A copy of tile t+2 and the
+  // W copy of tile t+2+XW, and the copies are ordered so that one wait for
+  // all but the last W copies covers both operands of tile t+1: A0, W0..WXW,
+  // A1, W(XW+1) up front, then A(t+2) W(t+2+XW) per crossing (copies
+  // complete in issue order).
+  auto kclamp = [&](int k) { return k < nk ? k : nk - 1; };
+  if constexpr (XW == 0) {
 #pragma unroll
-  for (int s0 = 0; s0 < NST; ++s0) issue(s0 < nk ? s0 : nk - 1, s0, skip_tag);
+    for (int s0 = 0; s0 < NST; ++s0) {
+      issue_a(kclamp(s0), s0, skip_tag);
+      issue_b(kclamp(s0), s0);
+    }
+  } else {
+    issue_a(0, 0, skip_tag);
+#pragma unroll
+    for (int s0 = 0; s0 <= XW; ++s0) issue_b(kclamp(s0), s0);
+    issue_a(kclamp(1), 1, skip_tag);
+    issue_b(kclamp(XW + 1), XW + 1);
+  }
   // (a wave that may have skipped copies has fewer in flight: it waits for all)
   if constexpr (SKIP) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  else asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NST - 1) * INS) : "memory");
+  else if constexpr (XW == 0) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NST - 1) * INS) : "memory");
+  else asm volatile("s_waitcnt vmcnt(%0)" ::"n"(A_INS + (XW + 1) * B_INS) : "memory");
   __syncthreads();
-  load_frags(smem, 0, 0);
-  int cur = 0;  // stage of tile kt
+  load_frags(stage_a(0), stage_b(0), 0, 0);
+  int ca = 0, cb = 0;  // stages of tile kt
   for (int kt = 0; kt + 1 < nk; ++kt) {
-    inner_steps(smem + cur * STAGE);
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NST - 2) * INS) : "memory");
+    inner_steps(stage_a(ca), stage_b(cb));
+    if constexpr (XW == 0) asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NST - 2) * INS) : "memory");
+    else asm volatile("s_waitcnt vmcnt(%0)" ::"n"(B_INS) : "memory");
     __syncthreads();
-    issue(kt + NST < nk ? kt + NST : nk - 1, cur, skip_tag);
-    cur = cur + 1 == NST ? 0 : cur + 1;
-    load_frags(smem + cur * STAGE, 0, 0);
+    issue_a(kclamp(kt + NST), ca, skip_tag);
+    issue_b(kclamp(kt + NSB), cb);
+    ca = ca + 1 == NST ? 0 : ca + 1;
+    cb = cb + 1 == NSB ? 0 : cb + 1;
+    load_frags(stage_a(ca), stage_b(cb), 0, 0);
     mfmas((KS - 1) & 1);
     if constexpr (NR > 0) {
       __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
       __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
     }
   }
-  inner_steps(smem + cur * STAGE);
+  inner_steps(stage_a(ca), stage_b(cb));
   mfmas((KS - 1) & 1);
   };  // pipeline
 
@@ -803,7 +833,7 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
   const int rowb = m0 + wm * WTM, colb = n0 + wn * WTN;
   if constexpr (EPI == EPI_RESIDUAL) {
     // a wave's LDS region holds one 32-row fp32 block of its tile
-    constexpr bool STAGED = NW * 32 * WTN * 2 <= NST * STAGE;
+    constexpr bool STAGED = NW * 32 * WTN * 2 <= LDS_ELEMS;
     if constexpr (STAGED) {
       float* ws = reinterpret_cast<float*>(smem + wave * (32 * WTN * 2));
       // (the batched x loads need 64 registers beside the accumulators: only
@@ -838,7 +868,7 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
   else if constexpr (EPI == EPI_SWIGLU) epi_swiglu<FM, FN>(c, acc, rowb, colb, lane);
   else if constexpr (EPI == EPI_QKV_ROPE) {
     // each wave stages its WTM x WTN tile in its own LDS region
-    static_assert(BM * BN <= NST * STAGE, "QKV staging fits the pipeline LDS");
+    static_assert(BM * BN <= LDS_ELEMS, "QKV staging fits the pipeline LDS");
     if (c.geom.T >= WTM) epi_qkv_rope<FM, FN, true>(c, acc, rowb, colb, lane, smem + wave * (WTM * WTN));
     else epi_qkv_rope<FM, FN, false>(c, acc, rowb, colb, lane, smem + wave * (WTM * WTN));
   }
@@ -851,6 +881,7 @@ struct TileCfg {
   int occ;      // workgroups a CU holds at once (LDS / registers)
   float eff;    // relative per-CU matrix-core throughput when the chip is full
                 // (measured on the 8704x24576x4096 gate/up shape)
+  int xw = 0;   // 1: a third LDS stage for the W tiles
 };
 
 // eff: measured relative throughput of each shape (8704 x 24576 x 4096, and
@@ -877,6 +908,8 @@ constexpr TileCfg kTiles[] = {
     {128, 256, 2, 4, 64, 2, 1, 0.74f},  // 8  (8 waves)
     {128, 256, 4, 2, 64, 2, 1, 0.77f},  // 9  (8 waves, 32-row wave tiles)
     {128, 256, 4, 2, 64, 3, 1, 0.78f},  // 10 (8 waves, three stages)
+    {256, 256, 4, 2, 64, 2, 1, 1.00f, 1},  // 11 (8 waves, third W stage)
+    {128, 256, 4, 2, 64, 2, 1, 0.77f, 1},  // 12 (8 waves, third W stage)
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 
@@ -896,8 +929,10 @@ bool tile_ok(const GemmCall& c, const TileCfg& t) {
   if (c.N % t.BN || c.K % BK) return false;
   if (!tile_epi(t.BM, t.BN, t.WM, t.WN, c.epi)) return false;
   const int arows = (c.epi == EPI_LMSTATS || c.epi == EPI_LOGITS) ? 2 * t.BM : t.BM;
-  if (t.occ * t.NST * (arows + t.BN) * t.KB * 2 > 160 * 1024) return false;
-  if (c.epi == EPI_QKV_ROPE && t.BM * t.BN > t.NST * (t.BM + t.BN) * t.KB) return false;
+  const int lds_elems = (t.NST * arows + (t.NST + t.xw) * t.BN) * t.KB;
+  if (t.xw && (arows != t.BM || t.NST != 2)) return false;
+  if (t.occ * lds_elems * 2 > 160 * 1024) return false;
+  if (c.epi == EPI_QKV_ROPE && t.BM * t.BN > lds_elems) return false;
   const int WTN = t.BN / t.WN;
   if (c.epi == EPI_QKV_ROPE) return WTN == c.rope.hd && (c.rope.H * c.rope.hd) % t.BN == 0;
   if (c.epi == EPI_SWIGLU) return (c.F % (WTN / 2)) == 0;
@@ -938,6 +973,20 @@ double makespan(long n_main, double T, long n_units, double U, long slots) {
   return std::max(main_end, best);
 }
 
+// eff of a tile for a unit of ksteps 64-deep K steps.  A W strip is read by
+// the ceil(M / BM) row tiles of its column; at five or fewer most of its
+// copies miss L2 and a two-stage pipeline waits on them, which a third W
+// stage covers once the unit is long enough to fill it (weights streamed
+// from HBM; 544 rows: 256x256 gate/up 138 -> 116 us, 128x256 down 72 -> 65
+// us, QKV 70 -> 67 us; 512 rows: gate/up 141 -> 103 us).  Where the
+// weights are shared by many row tiles (8704 rows: -1%) or the unit is short
+// (K slices of 8-16 steps: 10-17% slower) it does not pay.
+double eff_of(const GemmCall& c, const TileCfg& t, int ksteps) {
+  if (!t.xw) return t.eff;
+  const bool cold = (c.M + t.BM - 1) / t.BM <= 5;
+  return cold && ksteps >= 24 ? 1.2 * t.eff : 0.9 * t.eff;
+}
+
 // Time of the partial last row tile (rem = M mod BM rows) relative to a full
 // one.  8-wave shapes skip the MFMAs of rows past M per wave (the kernel's
 // rule: a wave keeps all its 32-row blocks, only the first, or none), so the
@@ -946,7 +995,7 @@ double makespan(long n_main, double T, long n_units, double U, long slots) {
 constexpr double kPartialFloor = 0.3;
 double partial_share(const GemmCall& c, const TileCfg& t, int rem) {
   const bool lm = c.epi == EPI_LMSTATS || c.epi == EPI_LOGITS;
-  if (rem == 0 || lm || t.WM * t.WN != 8 || t.NST != 2) return 1.0;
+  if (rem == 0 || lm || t.WM * t.WN != 8 || t.NST != 2) return 1.0;  // (XW tiles skip too)
   const int WTM = t.BM / t.WM, FM = WTM / 32;
   double load[4] = {0, 0, 0, 0};
   for (int w = 0; w < 8; ++w) {
@@ -967,7 +1016,7 @@ double tile_time(const GemmCall& c, const TileCfg& t) {
   const long n_full = (long)(c.M / t.BM) * nTN, n_part = rem ? nTN : 0;
   const long per_cu = std::min<long>(t.occ, (n_full + n_part + 255) / 256);
   const double util = 0.5 + 0.5 * (double)per_cu / t.occ;
-  const double tile_s = 2.0 * t.BM * t.BN * (double)c.K / (t.eff * util * kCuFlops);
+  const double tile_s = 2.0 * t.BM * t.BN * (double)c.K / (eff_of(c, t, c.K / BK) * util * kCuFlops);
   return makespan(n_full, tile_s, n_part, partial_share(c, t, rem) * tile_s, 256);
 }
 
@@ -977,7 +1026,7 @@ double tile_time(const GemmCall& c, const TileCfg& t) {
 double residual_time(const GemmCall& c, const TileCfg& t, int tail_tm, int splits) {
   const int nTM = (c.M + t.BM - 1) / t.BM, nTN = c.N / t.BN;
   const long slots = 256L * t.occ;
-  const double rate = t.eff * kCuFlops / t.occ;
+  const double rate = eff_of(c, t, c.K / BK) * kCuFlops / t.occ;
   const double out_s = (double)t.BM * t.BN / (kEpiBw / slots);
   const double T = 2.0 * t.BM * t.BN * (double)c.K / rate + 8.0 * out_s;
   const long n_main = (long)(nTM - tail_tm) * nTN;
@@ -985,7 +1034,8 @@ double residual_time(const GemmCall& c, const TileCfg& t, int tail_tm, int split
     const int rem = c.M % t.BM;
     return makespan(n_main - (rem ? nTN : 0), T, rem ? nTN : 0, partial_share(c, t, rem) * T, slots);
   }
-  const double U = 2.0 * t.BM * t.BN * ((double)c.K / splits + 2 * BK) / rate + 4.0 * out_s;
+  const double urate = eff_of(c, t, c.K / splits / BK) * kCuFlops / t.occ;
+  const double U = 2.0 * t.BM * t.BN * ((double)c.K / splits + 2 * BK) / urate + 4.0 * out_s;
   const long n_units = (long)tail_tm * nTN * splits;
   const double tail_rows = c.M - (double)(nTM - tail_tm) * t.BM;
   return makespan(n_main, T, n_units, U, slots) + splits * tail_rows * c.N * 4.0 / kPartBw;
@@ -1009,34 +1059,36 @@ std::mutex g_plan_mu;
 PlanEntry g_plans[32];
 int g_n_plans = 0;
 
-template <int BM, int BN, int WM, int WN, int EPI, int KB, int NST, int OCC>
+template <int BM, int BN, int WM, int WN, int EPI, int KB, int NST, int OCC, int XW>
 hipError_t launch_one(const GemmCall& c, hipStream_t st) {
-  constexpr int arows = (EPI == EPI_LMSTATS || EPI == EPI_LOGITS) ? 2 * BM : BM;
-  constexpr int lds = NST * (arows + BN) * KB * 2;
-  constexpr bool qkv_fits = EPI != EPI_QKV_ROPE || BM * BN <= NST * (BM + BN) * KB;
-  if constexpr (tile_epi(BM, BN, WM, WN, EPI) && lds * OCC <= 160 * 1024 && qkv_fits) {
+  constexpr bool split = EPI == EPI_LMSTATS || EPI == EPI_LOGITS;
+  constexpr int arows = split ? 2 * BM : BM;
+  constexpr int lds = (NST * arows + (NST + XW) * BN) * KB * 2;
+  constexpr bool qkv_fits = EPI != EPI_QKV_ROPE || BM * BN * 2 <= lds;
+  if constexpr (tile_epi(BM, BN, WM, WN, EPI) && lds * OCC <= 160 * 1024 && qkv_fits &&
+                (XW == 0 || !split)) {
     const int nTM = (c.M + BM - 1) / BM, nTN = c.N / BN;
     int units = nTM * nTN;
     if (EPI == EPI_RESIDUAL && c.splits > 1) {
       const int mainTM = c.split_row0 / BM;
       units = mainTM * nTN + (nTM - mainTM) * nTN * c.splits;
     }
-    gemm_kernel<BM, BN, WM, WN, EPI, KB, NST, OCC><<<dim3(units), dim3(WM * WN * 64), 0, st>>>(c);
+    gemm_kernel<BM, BN, WM, WN, EPI, KB, NST, OCC, XW><<<dim3(units), dim3(WM * WN * 64), 0, st>>>(c);
     return hipGetLastError();
   } else {
     return hipErrorInvalidValue;
   }
 }
 
-template <int BM, int BN, int WM, int WN, int KB, int NST, int OCC>
+template <int BM, int BN, int WM, int WN, int KB, int NST, int OCC, int XW = 0>
 hipError_t launch_cfg(const GemmCall& c, hipStream_t st) {
   switch (c.epi) {
-    case EPI_QKV_ROPE: return launch_one<BM, BN, WM, WN, EPI_QKV_ROPE, KB, NST, OCC>(c, st);
-    case EPI_RESIDUAL: return launch_one<BM, BN, WM, WN, EPI_RESIDUAL, KB, NST, OCC>(c, st);
-    case EPI_SWIGLU: return launch_one<BM, BN, WM, WN, EPI_SWIGLU, KB, NST, OCC>(c, st);
-    case EPI_LMSTATS: return launch_one<BM, BN, WM, WN, EPI_LMSTATS, KB, NST, OCC>(c, st);
-    case EPI_STORE_F32: return launch_one<BM, BN, WM, WN, EPI_STORE_F32, KB, NST, OCC>(c, st);
-    case EPI_LOGITS: return launch_one<BM, BN, WM, WN, EPI_LOGITS, KB, NST, OCC>(c, st);
+    case EPI_QKV_ROPE: return launch_one<BM, BN, WM, WN, EPI_QKV_ROPE, KB, NST, OCC, XW>(c, st);
+    case EPI_RESIDUAL: return launch_one<BM, BN, WM, WN, EPI_RESIDUAL, KB, NST, OCC, XW>(c, st);
+    case EPI_SWIGLU: return launch_one<BM, BN, WM, WN, EPI_SWIGLU, KB, NST, OCC, XW>(c, st);
+    case EPI_LMSTATS: return launch_one<BM, BN, WM, WN, EPI_LMSTATS, KB, NST, OCC, XW>(c, st);
+    case EPI_STORE_F32: return launch_one<BM, BN, WM, WN, EPI_STORE_F32, KB, NST, OCC, XW>(c, st);
+    case EPI_LOGITS: return launch_one<BM, BN, WM, WN, EPI_LOGITS, KB, NST, OCC, XW>(c, st);
   }
   return hipErrorInvalidValue;
 }
@@ -1118,6 +1170,8 @@ hipError_t launch_gemm(const GemmCall& c, hipStream_t st) {
     case 8: return launch_cfg<128, 256, 2, 4, 64, 2, 1>(c, st);
     case 9: return launch_cfg<128, 256, 4, 2, 64, 2, 1>(c, st);
     case 10: return launch_cfg<128, 256, 4, 2, 64, 3, 1>(c, st);
+    case 11: return launch_cfg<256, 256, 4, 2, 64, 2, 1, 1>(c, st);
+    case 12: return launch_cfg<128, 256, 4, 2, 64, 2, 1, 1>(c, st);
   }
   return hipErrorInvalidValue;
 }
