@@ -918,11 +918,13 @@ constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 // 128x256 tile: 1.19 -> 0.97 ms for the 512-row LM head); the thin 32-row
 // tile serves only them (it loses to wider tiles elsewhere); the 4-wave
 // 256x256 tile spills registers in the RoPE epilogue.  (RoPE also needs a
-// wave to own exactly one head, WTN == hd: checked per call.)
+// wave to own exactly one head, WTN == hd: 64 or 128 here, checked per call.)
 constexpr bool tile_epi(int BM, int BN, int WM, int WN, int EPI) {
   return (EPI == EPI_LMSTATS || EPI == EPI_LOGITS)
              ? (BM == 32 || (BM == 128 && BN == 256))
-             : (BM != 32 && (EPI == EPI_QKV_ROPE ? !(BM == 256 && WM == 2 && WN == 2) : true));
+             : (BM != 32 && (EPI == EPI_QKV_ROPE ? !(BM == 256 && WM == 2 && WN == 2) &&
+                                                       (BN / WN == 64 || BN / WN == 128)
+                                                 : true));
 }
 
 bool tile_ok(const GemmCall& c, const TileCfg& t) {
