@@ -699,6 +699,35 @@ def test_step_is_deterministic(P):
     model.close()
 
 
+# ---------------------------------------------------------------- GEMM tiles
+@pytest.mark.parametrize("M,N,K", [(544, 512, 4096), (100, 512, 1024), (1, 256, 256)])
+def test_gemm_tiles_within_exact_product_bound(P, M, N, K, monkeypatch):
+    """Each entry of the GEMM tile table, forced through WINO_GEMM_TILE (an
+    entry that cannot serve the call falls back to the planner's choice),
+    against the float64 sum of the same bf16 products.  Products of bf16
+    values are exact in fp32, so any order of fp32 additions stays within
+    (K-1)*2^-24 * sum|a*w| of that sum.  Ragged M (544 = 2*256 + 32, 100, 1)
+    covers the partial row tiles whose waves skip rows past M.  The tiles
+    with a third W stage change only when the copies land: they reproduce
+    their two-stage twins (entries 6 and 9) bit for bit."""
+    gen = torch.Generator().manual_seed(M * 7 + K)
+    A = torch.randn(M, K, generator=gen).bfloat16()
+    Wt = (torch.randn(N, K, generator=gen) * 0.02).bfloat16()
+    ref = A.double() @ Wt.double().T
+    bound = (K - 1) * 2.0 ** -24 * (A.double().abs() @ Wt.double().abs().T)
+    Ad, Wd = A.cuda(), Wt.cuda()
+    outs = {}
+    for t in range(16):
+        monkeypatch.setenv("WINO_GEMM_TILE", str(t))
+        out = torch.full((M, N), float("nan"), device="cuda")
+        P.wino_debug_gemm(Ad, Wd, out)
+        torch.cuda.synchronize()
+        outs[t] = out.cpu()
+        err = (outs[t].double() - ref).abs()
+        assert bool((err <= bound).all()), (t, float((err / bound.clamp_min(1e-300)).max()))
+    assert torch.equal(outs[6], outs[11]) and torch.equal(outs[9], outs[12])
+
+
 # ---------------------------------------------------------------- standalone epilogue
 @pytest.mark.parametrize("B,lb,V,heights", [(2, 8, 4096, (10.0, 16.0)), (8, 32, 126464, (10.0, 16.0)),
                                             (8, 32, 126464, (0.0, 12.0)), (3, 5, 1000, (0.0, 14.0))])
