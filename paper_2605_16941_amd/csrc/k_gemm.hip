@@ -631,7 +631,8 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
   // only the first wait changes.
   constexpr bool CAN_SKIP = NST == 2 && !SPLIT && NW == 8;  // (W copies are never skipped)
   constexpr bool BIG2 = NW == 8 && BM == 256 && BN == 256 && XW == 0;
-  constexpr int CROSS = !BIG2 ? 1 : EPI == EPI_QKV_ROPE ? 2 : (EPI == EPI_SWIGLU || EPI == EPI_RESIDUAL) ? 0 : 1;
+  constexpr int CROSS = BIG2 ? 3 : 1;
+  static_assert(CROSS != 3 || (XW == 0 && NST == 2), "the W-first crossing relies on waiting for every copy");
   bool alive[A_INS];
   const uint16_t* asrc[A_INS];
 #pragma unroll
@@ -768,12 +769,13 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
   // has read all of tile t, (3) issues the first fragment reads of tile t+1
   // and tile t+NST's copy into tile t's stage, and (4) runs the last MFMAs
   // of tile t, which cover the latency of those reads.  The order of the
-  // reads, the copy and the MFMAs at that crossing (CROSS) is measured per
-  // tile: 1 = reads, copy, MFMAs (544-row gate/up 112 -> 100 us against 0);
-  // 0 = copy, reads, MFMAs (0.6-2% ahead of 1 in the two-stage 8-wave
-  // 256x256 SwiGLU and residual tiles); 2 = reads, MFMAs, copy (the same
-  // tile with the QKV epilogue: 8704 rows 755 (0) -> 735 (1) -> 712 us; it
-  // loses 3-10% wherever the weights come from HBM).  Tiles past
+  // reads, the copies and the MFMAs at that crossing (CROSS) is measured per
+  // tile against copies-then-reads: 1 = reads, copies, MFMAs (544-row
+  // gate/up 112 -> 100 us); 3 = W copy, reads, A copy, MFMAs for the
+  // two-stage 8-wave 256x256 tile (8704 rows: gate/up 1378 -> 1348 us, down
+  // 721 -> 710 us, QKV 755 -> 689 us).  3 needs the wait for every copy of
+  // the two-stage tile: with a third W stage the waits count on A copies
+  // being issued before W copies at each crossing.  Tiles past
   // the end are refetches of the last one, which keeps the wait counts fixed.
   // With XW extra W stages the crossing issues the A copy of tile t+2 and the
   // W copy of tile t+2+XW, and the copies are ordered so that one wait for
@@ -807,20 +809,15 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
     else asm volatile("s_waitcnt vmcnt(%0)" ::"n"(B_INS) : "memory");
     __syncthreads();
     const int na = ca + 1 == NST ? 0 : ca + 1, nb = cb + 1 == NSB ? 0 : cb + 1;
-    if constexpr (CROSS != 0) load_frags(stage_a(na), stage_b(nb), 0, 0);
-    if constexpr (CROSS != 2) {
-      issue_a(kclamp(kt + NST), ca, skip_tag);
-      issue_b(kclamp(kt + NSB), cb);
-    }
-    if constexpr (CROSS == 0) load_frags(stage_a(na), stage_b(nb), 0, 0);
+    if constexpr (CROSS == 3) issue_b(kclamp(kt + NSB), cb);
+    load_frags(stage_a(na), stage_b(nb), 0, 0);
+    if constexpr (CROSS == 1) issue_a(kclamp(kt + NST), ca, skip_tag);
+    if constexpr (CROSS == 1) issue_b(kclamp(kt + NSB), cb);
+    if constexpr (CROSS == 3) issue_a(kclamp(kt + NST), ca, skip_tag);
     mfmas((KS - 1) & 1);
     if constexpr (NR > 0) {
       __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
       __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
-    }
-    if constexpr (CROSS == 2) {
-      issue_a(kclamp(kt + NST), ca, skip_tag);
-      issue_b(kclamp(kt + NSB), cb);
     }
     ca = na;
     cb = nb;
