@@ -41,7 +41,7 @@ __device__ __forceinline__ int perm_key(int r) {
 // CQ (compact queries): only each sequence's current-block rows and shadow
 // rows are queried - compact query i < Lb is row c0 + i, i >= Lb is row
 // S + i - Lb - and output row i of sequence b goes to o row b*(Lb+Ls) + i.
-template <int HD, int NW, bool CQ>
+template <int HD, int NW, bool CQ, int NS>
 __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const uint16_t* __restrict__ q,
                                                        const uint16_t* __restrict__ k,
                                                        const uint16_t* __restrict__ vt, int H,
@@ -55,7 +55,8 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
   static_assert(K_INS * KROWS * NW == BKV && V_INS * 8 * NW == HD, "loader split");
   constexpr int KTILE = BKV * HD;    // bf16 elements
   constexpr int STAGE = 2 * KTILE;   // K tile then V^T tile
-  __shared__ __attribute__((aligned(1024))) uint16_t smem[2 * STAGE];
+  static_assert(NS >= 2, "pipeline stages");
+  __shared__ __attribute__((aligned(1024))) uint16_t smem[NS * STAGE];
 
   const int b = blockIdx.z, h = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, grp = lane >> 5;
@@ -149,16 +150,21 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
     vswz[fe] = (e ^ (e >> 3)) & 7;
   }
 
-  issue(0, 0);
+  // The copies of tile t are issued NS-1 tiles ahead, into stage t % NS; with
+  // more than two stages the tiles past the last are fetches of the last one
+  // again, which keeps the number of copies in flight fixed.
+#pragma unroll
+  for (int s0 = 0; s0 + 1 < NS; ++s0) issue(min(s0, ntile - 1) * BKV, s0);
   for (int t = 0; t < ntile; ++t) {
     const int kv0 = t * BKV;
-    // own copies of tile t landed; after the barrier everyone's have, and
-    // everyone finished tile t-1, whose stage tile t+1 may now overwrite
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // own copies of tile t landed (the NS-2 tiles after it may still be in
+    // flight); after the barrier everyone's have, and everyone finished tile
+    // t-1, whose stage tile t+NS-1 may now overwrite
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"((NS - 2) * (K_INS + V_INS)) : "memory");
     __syncthreads();
-    if (t + 1 < ntile) issue(kv0 + BKV, (t + 1) & 1);
+    if (NS > 2 || t + 1 < ntile) issue(min(t + NS - 1, ntile - 1) * BKV, (t + NS - 1) % NS);
     if (!wave_live) continue;
-    const uint16_t* sK = smem + (t & 1) * STAGE;
+    const uint16_t* sK = smem + (t % NS) * STAGE;
     const uint16_t* sV = sK + KTILE;
 
     // S^T for the two 32-key blocks: the two MFMA chains alternate, and the
@@ -281,19 +287,15 @@ hipError_t launch_hd(const StepGeom& g, const uint16_t* q, const uint16_t* k, co
                      int H, uint16_t* o, float scale_log2, bool compact, hipStream_t st) {
   if (compact) {
     dim3 grid((g.Lb + g.Ls + 63) / 64, H, g.B);
-    attn_kernel<HD, 2, true><<<grid, 128, 0, st>>>(g, q, k, vt, H, o, scale_log2);
+    attn_kernel<HD, 2, true, 2><<<grid, 128, 0, st>>>(g, q, k, vt, H, o, scale_log2);
     return hipGetLastError();
   }
-  // 128-query workgroups when there are enough of them to fill the chip,
-  // otherwise 64-query ones (more workgroups per head).
-  const long wg128 = (long)((g.T + 127) / 128) * H * g.B;
-  if (wg128 >= 512) {
-    dim3 grid((g.T + 127) / 128, H, g.B);
-    attn_kernel<HD, 4, false><<<grid, 256, 0, st>>>(g, q, k, vt, H, o, scale_log2);
-  } else {
-    dim3 grid((g.T + 63) / 64, H, g.B);
-    attn_kernel<HD, 2, false><<<grid, 128, 0, st>>>(g, q, k, vt, H, o, scale_log2);
-  }
+  // 128-query workgroups (four waves) at every size: at 544 rows they take
+  // 16.6 us against 21.3 us for twice as many 64-query workgroups (whose
+  // two-wave kernel spends 96 accumulation registers and runs one wave per
+  // SIMD), and three or four K/V stages did not pay there either.
+  dim3 grid((g.T + 127) / 128, H, g.B);
+  attn_kernel<HD, 4, false, 2><<<grid, 256, 0, st>>>(g, q, k, vt, H, o, scale_log2);
   return hipGetLastError();
 }
 
