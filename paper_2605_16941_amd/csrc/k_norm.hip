@@ -172,10 +172,13 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x,
 }
 
 // RMSNorm with a whole workgroup per row (d = 2048 * CPT): 256 threads hold
-// CPT 8-element chunks each, so a row's loads (x and every partial) are all in
-// flight at once.  Against one wave per row: 6.3 vs 4.7 TB/s at 8704 x 4096,
-// and 11 vs 17 us per launch at 544 rows.
-template <int CPT>
+// CPT 8-element chunks each, so a row's loads (x, every partial and the gain)
+// are all in flight at once.  Against one wave per row: 6.3 vs 4.7 TB/s at
+// 8704 x 4096, and 11 vs 17 us per launch at 544 rows.  NP is the number of
+// split-K partials when known at compile time (their loads are then all
+// issued before the first wait; -1: a runtime loop over them, one round trip
+// each), added in split order either way.
+template <int CPT, int NP>
 __global__ __launch_bounds__(256) void rmsnorm_row_kernel(float* __restrict__ x,
                                                           const uint16_t* __restrict__ gain, float eps,
                                                           int M, int d, uint16_t* __restrict__ h,
@@ -189,24 +192,43 @@ __global__ __launch_bounds__(256) void rmsnorm_row_kernel(float* __restrict__ x,
   const bool has = n_part && m >= part_row0;
   float* xr = x + (size_t)m * d;
   float v[CPT][8];
+  uint4 graw[CPT];
 #pragma unroll
   for (int c = 0; c < CPT; ++c) {
     const float4* xi = reinterpret_cast<const float4*>(xr + (c * 256 + tid) * 8);
     const float4 a = xi[0], b = xi[1];
     v[c][0] = a.x; v[c][1] = a.y; v[c][2] = a.z; v[c][3] = a.w;
     v[c][4] = b.x; v[c][5] = b.y; v[c][6] = b.z; v[c][7] = b.w;
+    graw[c] = *reinterpret_cast<const uint4*>(gain + (c * 256 + tid) * 8);
   }
+  auto add = [&](int c, float4 a, float4 b) {
+    v[c][0] += a.x; v[c][1] += a.y; v[c][2] += a.z; v[c][3] += a.w;
+    v[c][4] += b.x; v[c][5] += b.y; v[c][6] += b.z; v[c][7] += b.w;
+  };
   if (has) {
     const float* pr = part + (size_t)(m - part_row0) * d;
     const size_t pstride = (size_t)(M - part_row0) * d;
-    for (int s = 0; s < n_part; ++s) {
+    if constexpr (NP > 0) {
+      float4 pa[NP][CPT][2];
 #pragma unroll
-      for (int c = 0; c < CPT; ++c) {
-        const float4* pi = reinterpret_cast<const float4*>(pr + s * pstride + (c * 256 + tid) * 8);
-        const float4 a = pi[0], b = pi[1];
-        v[c][0] += a.x; v[c][1] += a.y; v[c][2] += a.z; v[c][3] += a.w;
-        v[c][4] += b.x; v[c][5] += b.y; v[c][6] += b.z; v[c][7] += b.w;
-      }
+      for (int s = 0; s < NP; ++s)
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) {
+          const float4* pi = reinterpret_cast<const float4*>(pr + s * pstride + (c * 256 + tid) * 8);
+          pa[s][c][0] = pi[0];
+          pa[s][c][1] = pi[1];
+        }
+#pragma unroll
+      for (int s = 0; s < NP; ++s)
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) add(c, pa[s][c][0], pa[s][c][1]);
+    } else if constexpr (NP < 0) {
+      for (int s = 0; s < n_part; ++s)
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) {
+          const float4* pi = reinterpret_cast<const float4*>(pr + s * pstride + (c * 256 + tid) * 8);
+          add(c, pi[0], pi[1]);
+        }
     }
 #pragma unroll
     for (int c = 0; c < CPT; ++c) {
@@ -229,8 +251,7 @@ __global__ __launch_bounds__(256) void rmsnorm_row_kernel(float* __restrict__ x,
 #pragma unroll
   for (int c = 0; c < CPT; ++c) {
     const int ch = c * 256 + tid;
-    const uint4 graw = *reinterpret_cast<const uint4*>(gain + ch * 8);
-    const uint16_t* gp = reinterpret_cast<const uint16_t*>(&graw);
+    const uint16_t* gp = reinterpret_cast<const uint16_t*>(&graw[c]);
     uint4 o;
     uint32_t* op = reinterpret_cast<uint32_t*>(&o);
 #pragma unroll
@@ -318,13 +339,27 @@ void launch_embed_norm(const StepGeom& g, const int32_t* tokens, const uint16_t*
   else embed_norm_kernel<8><<<grid, block, 0, st>>>(g, tokens, emb, vocab, gain, eps, d, x, h);
 }
 
+template <int CPT>
+void launch_row_norm(float* x, const uint16_t* gain, float eps, int M, int d, uint16_t* h,
+                     const float* part, int n_part, int part_row0, hipStream_t st) {
+  // the split counts the residual planner uses get their own instance
+  switch (n_part) {
+    case 0: rmsnorm_row_kernel<CPT, 0><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0); break;
+    case 2: rmsnorm_row_kernel<CPT, 2><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0); break;
+    case 3: rmsnorm_row_kernel<CPT, 3><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0); break;
+    case 4: rmsnorm_row_kernel<CPT, 4><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0); break;
+    case 8: rmsnorm_row_kernel<CPT, 8><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0); break;
+    default: rmsnorm_row_kernel<CPT, -1><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
+  }
+}
+
 void launch_rmsnorm(float* x, const uint16_t* gain, float eps, int M, int d, uint16_t* h,
                     const float* part, int n_part, int part_row0, hipStream_t st) {
   const dim3 grid((M + 3) / 4), block(256);
   if (!part) n_part = 0;
   if (d == 2048 || d == 4096) {  // measured faster at 544 and 8704 rows
-    if (d == 2048) rmsnorm_row_kernel<1><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
-    else rmsnorm_row_kernel<2><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
+    if (d == 2048) launch_row_norm<1>(x, gain, eps, M, d, h, part, n_part, part_row0, st);
+    else launch_row_norm<2>(x, gain, eps, M, d, h, part, n_part, part_row0, st);
     return;
   }
   if (d <= 512) rmsnorm_kernel<1><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
