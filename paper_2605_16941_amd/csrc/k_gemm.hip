@@ -772,8 +772,8 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
   // reads, the copies and the MFMAs at that crossing (CROSS) is measured per
   // tile against copies-then-reads: 1 = reads, copies, MFMAs (544-row
   // gate/up 112 -> 100 us); 3 = W copy, reads, A copy, MFMAs for the
-  // two-stage 8-wave 256x256 tile (8704 rows: gate/up 1378 -> 1348 us, down
-  // 721 -> 710 us, QKV 755 -> 689 us).  3 needs the wait for every copy of
+  // two-stage 8-wave 256x256 tile (8704 rows, runs alternating with 1:
+  // gate/up 1359 -> 1339 us, QKV 724 -> 711 us, down 713 -> 702 us).  3 needs the wait for every copy of
   // the two-stage tile: with a third W stage the waits count on A copies
   // being issued before W copies at each crossing.  Tiles past
   // the end are refetches of the last one, which keeps the wait counts fixed.
