@@ -159,21 +159,35 @@ wino_status wino_decode_block(wino_ctx* ctx, const wino_params* p, int32_t* d_to
                               int32_t* h_steps, void* stream);
 
 /* Full semi-autoregressive decode (Sec. 3): every sequence advances to its
- * next block as soon as its current block holds no mask; returns when all
- * sequences reach gen_len.  Resumable: d_block_start [batch] gives each
- * sequence's starting block and ends at gen_len.  d_final_step int32
- * [batch, gen_len] (device, or NULL) receives, for every response position
- * this call changes, the sequence's step (1-based, counted from this call)
- * at which the position last changed: from an all-mask response that is the
- * finalization step t_l of Sec. 4.3; positions never changed keep the
- * caller's values.  h_steps_per_seq [batch] (or NULL) receives the steps
- * each sequence took; h_forward_passes (or NULL) the number of batched
- * forwards.  Synchronises once per step. */
+ * next block as soon as its current block holds no mask (Sec. 4.2.3); a block
+ * that already holds no mask when the sequence reaches it (filled by the
+ * caller, or by an earlier call) is skipped without a forward.  Returns when
+ * every sequence reaches gen_len, or after max_forwards batched forwards.
+ *
+ * Resumable: the decode state is exactly (d_tokens, d_block_start,
+ * d_block_steps).  d_block_start int32 [batch] (in/out) is each sequence's
+ * current block, a multiple of block_len; gen_len means done.
+ * d_block_steps int32 [batch] (device, in/out, or NULL) holds the steps
+ * already taken in that block, which count toward the step cap; NULL starts
+ * every block count at 0.  max_forwards > 0 stops after that many batched
+ * forwards with WINO_OK, leaving a state from which a later call continues
+ * exactly as the uninterrupted decode would (0 = no limit).
+ *
+ * d_final_step int32 [batch, gen_len] (device, or NULL) receives, for every
+ * response position this call changes, the sequence's step (1-based, counted
+ * from this call) at which the position last changed: from an all-mask
+ * response that is the finalization step t_l of Sec. 5.1; positions never
+ * changed keep the caller's values.  h_steps_per_seq [batch] (or NULL)
+ * receives the steps each sequence took in this call; h_forward_passes (or
+ * NULL) the number of batched forwards.  Synchronises once per step.
+ * WINO_ERR_STEP_CAP: a block reached its cap with WINO_FLAG_NO_CAP_FILL set;
+ * the state is left at that step. */
 wino_status wino_decode(wino_ctx* ctx, const wino_params* p, int32_t* d_tokens,
-                        int32_t* d_block_start, int32_t* d_final_step, int32_t* h_steps_per_seq,
-                        int32_t* h_forward_passes, void* stream);
+                        int32_t* d_block_start, int32_t* d_block_steps, int32_t* d_final_step,
+                        int32_t max_forwards, int32_t* h_steps_per_seq, int32_t* h_forward_passes,
+                        void* stream);
 
-/* Per response position quantities of a WINO+ training state (Sec. 4.3). */
+/* Per response position quantities of a WINO+ training state (Sec. 5.2-5.3). */
 typedef struct {
   float entropy;  /* H(p) = -sum_v p(v) log p(v), p = softmax of the row's logits */
   float nll;      /* -log p(target)                                             */
@@ -181,7 +195,7 @@ typedef struct {
   int32_t argmax; /* greedy prediction: lowest id reaching conf                 */
 } wino_row_loss;
 
-/* The forward half of the WINO+ objective (Sec. 4.3, Eq. 6-7): for each
+/* The forward half of the WINO+ objective (Sec. 5.3, Eq. 6-7): for each
  * sequence, a plain bidirectional forward over the training state d_tokens
  * int32 [batch, prompt_len+gen_len] (no shadow block; block_len and the
  * thresholds are not used), then for every response position j the entropy

@@ -16,7 +16,7 @@ Everything is plain numpy in float64, computed straight from the definitions:
 * ``epilogue`` - the decision taken directly from given logits of the current
                  and shadow blocks (the standalone epilogue workload).
 * ``losses``   - per-row entropy, target log-likelihood and greedy confidence
-                 of a WINO+ training state (Sec. 4.3).
+                 of a WINO+ training state (Sec. 5.2-5.3).
 
 Readings of points the paper leaves open are stated where they are used.
 """

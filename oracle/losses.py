@@ -2,7 +2,7 @@
 
 Test infrastructure only (see the package docstring).
 
-Sec. 4.3 (trajectory consistency objective): for a training state - the
+Sec. 5.3 (trajectory consistency objective): for a training state (Sec. 5.2, Eq. 5) - the
 response with only the tokens finalized before step t revealed, everything
 else the mask token - the model's prediction p at each response position
 enters the losses through
@@ -48,7 +48,7 @@ def state_logits(weights, cfg, tokens, prompt_len: int, act_round=None):
 
 
 def training_state(final, t_fin, t: int, prompt_len: int, mask_id: int):
-    """Sec. 4.3: the state before step t reveals exactly the response tokens
+    """Sec. 5.2, Eq. 5: the state before step t reveals exactly the response tokens
     with finalization step t_l < t (the prompt always); the rest are masks."""
     final = np.asarray(final, dtype=np.int64)
     t_fin = np.asarray(t_fin, dtype=np.int64)

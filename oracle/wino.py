@@ -14,9 +14,9 @@ Paper passages followed:
   row's probability of the current token, p(y_shad,l = y_cur,l), is < tau2.
 * Sec. 4.2.3, Eq. 4: both rules read the previous state y^(k-1) and act in one
   forward; iterate until Y_cur has no mask token.
-* Sec. 4.3: a position's finalization step is the first step from which its
+* Sec. 5.1: a position's finalization step is the first step from which its
   token no longer changes (the WINO+ trajectory data).
-* Sec. 3 and the comparison with naive parallel sampling (Sec. 5): the
+* Sec. 3 and the comparison with naive parallel sampling (Sec. 6.3): the
   baselines unmask a fixed number M of tokens per step - the M most confident
   masked positions of the block, M = 1 being Eq. 1 - with no threshold and no
   verification (``tokens_per_step`` > 0 selects this mode; it needs no step
@@ -209,7 +209,7 @@ def decode_block(provider, tokens, prm: Params, block_start: int, trace=None):
 
 
 def finalization_steps(states, prompt_len: int) -> np.ndarray:
-    """Sec. 4.3 (verified trajectories): for the states Y^(0..K) of one
+    """Sec. 5.1 (verified trajectories): for the states Y^(0..K) of one
     sequence's decode, t_l = min{t : y_l^(j) = y_l^(K) for every j >= t};
     prompt positions get 0.  Written from the definition: scan t upward."""
     Y = np.asarray(states, dtype=np.int64)          # [K + 1, P + G]

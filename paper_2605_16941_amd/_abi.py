@@ -84,7 +84,7 @@ _protos = {
     "wino_workspace_bytes": (_sz, [_P(wino_model_config), _i32, _i32]),
     "wino_step": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "wino_decode_block": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _P(_i32), _vp]),
-    "wino_decode": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _P(_i32), _P(_i32), _vp]),
+    "wino_decode": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _vp, _i32, _P(_i32), _P(_i32), _vp]),
     "wino_epilogue_workspace_bytes": (_sz, [_i32, _i32, _i32]),
     "wino_epilogue": (_i32, [_P(wino_params), _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "wino_row_losses": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _vp]),
@@ -186,21 +186,26 @@ def wino_decode_block(ctx, p: wino_params, tokens, block_start, final_step=None,
     return list(steps)
 
 
-def wino_decode(ctx, p: wino_params, tokens, block_start, final_step=None, stream=None):
+def wino_decode(ctx, p: wino_params, tokens, block_start, final_step=None, stream=None,
+                block_steps=None, max_forwards=0):
     """Returns (per-sequence steps, batched forward passes).  final_step: int32
-    [batch, gen_len] device tensor for the finalization steps, or None."""
+    [batch, gen_len] device tensor for the finalization steps, or None;
+    block_steps: int32 [batch] device tensor (in/out) of steps already taken
+    in each current block, or None; max_forwards > 0 stops early with a
+    resumable state."""
     import torch
     steps = (C.c_int32 * p.batch)()
     fw = C.c_int32(0)
     fs = _ptr(final_step, torch.int32, "final_step") if final_step is not None else None
     _check(lib.wino_decode(ctx, C.byref(p), _ptr(tokens, torch.int32, "tokens"),
-                           _ptr(block_start, torch.int32, "block_start"), fs, steps, C.byref(fw),
-                           _stream(stream)), "wino_decode", ctx)
+                           _ptr(block_start, torch.int32, "block_start"),
+                           _ptr(block_steps, torch.int32, "block_steps"), fs, int(max_forwards), steps,
+                           C.byref(fw), _stream(stream)), "wino_decode", ctx)
     return list(steps), fw.value
 
 
 def wino_row_losses(ctx, p: wino_params, tokens, targets, out, stream=None) -> None:
-    """WINO+ per-row quantities of training states (Sec. 4.3).  tokens int32
+    """WINO+ per-row quantities of training states (Sec. 5.2-5.3).  tokens int32
     [B, P+G], targets int32 [B, G], out: device buffer of B*G wino_row_loss
     (16 bytes each: entropy, nll, conf float32; argmax int32)."""
     import torch

@@ -47,6 +47,56 @@ __device__ __forceinline__ Part group_merge(Part p, int gs) {
   return p;
 }
 
+// First response position in [from, G) of sequence b holding the mask, or G;
+// a block-wide minimum over 256 threads.
+__device__ int first_mask_from(const DecideArgs& a, int b, int from) {
+  __shared__ int s_first;
+  if (threadIdx.x == 0) s_first = a.G;
+  __syncthreads();
+  const int32_t* resp = a.tokens + (size_t)b * a.S + a.P;
+  for (int j = from + (int)threadIdx.x; j < a.G; j += 256)
+    if (resp[j] == a.mask_id) { atomicMin(&s_first, j); break; }
+  __syncthreads();
+  const int f = s_first;
+  __syncthreads();
+  return f;
+}
+
+// End of a fused step for an active sequence whose Y_cur holds nmask_after
+// masks.  In decode mode (advance) a sequence whose block holds no mask moves
+// to the first later block that still holds one - blocks filled beforehand
+// (a resumed or pre-filled state) are skipped - or to G when none is left
+// (Sec. 3: blocks left to right; Sec. 4.2.3: a block ends when Y_cur holds no
+// mask), and its block step count restarts.  next_verify then describes the
+// Y_cur the next step will see.  All 256 threads call this.
+__device__ void advance_block(const DecideArgs& a, int b, int nmask_after) {
+  __shared__ int s_m, s_k;
+  const int bs = a.block_start[b];
+  int nbs = bs;
+  if (a.advance && nmask_after == 0 && bs < a.G) {
+    const int f = first_mask_from(a, b, bs + a.Lb);
+    nbs = f >= a.G ? a.G : bs + (f - bs) / a.Lb * a.Lb;
+  }
+  if (a.next_verify) {
+    if (threadIdx.x == 0) { s_m = 0; s_k = 0; }
+    __syncthreads();
+    if (nbs < a.G) {
+      const int c = nbs > a.G - a.Lb ? a.G - a.Lb : nbs;
+      const int32_t* nxt = a.tokens + (size_t)b * a.S + a.P + c;
+      for (int l = threadIdx.x; l < a.Lb; l += 256) {
+        if (nxt[l] == a.mask_id) atomicAdd(&s_m, 1);
+        else atomicAdd(&s_k, 1);
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) a.next_verify[b] = s_m > 0 && s_k > 0;
+  }
+  if (threadIdx.x == 0 && nbs != bs) {
+    a.block_start[b] = nbs;
+    if (a.block_steps) a.block_steps[b] = 0;
+  }
+}
+
 __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
   extern __shared__ int smem_i[];
   int* s_cur = smem_i;                                   // [Lb] token before the step
@@ -82,7 +132,8 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
     }
   }
   __syncthreads();
-  // A finished sequence, or (fused step) a block with no mask left, is idle.
+  // A finished sequence, or (fused step) a block with no mask left, is idle:
+  // no decision, and in decode mode it only moves on to its next block below.
   const bool idle = done || (!a.standalone && s_nmask == 0);
   if (idle) {
     for (int l = tid; l < Lb; l += 256) {
@@ -94,7 +145,11 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
       }
     }
     if (tid == 0 && a.n_masked) a.n_masked[b] = 0;
-    if (tid == 0 && a.next_verify) a.next_verify[b] = 0;
+    if (done) {
+      if (tid == 0 && a.next_verify) a.next_verify[b] = 0;
+      return;
+    }
+    advance_block(a, b, 0);
     return;
   }
 
@@ -187,57 +242,59 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
     else if (f == WINO_REMASK_FLAG) t = a.mask_id;
     if (t != s_cur[l]) {
       cur_ptr[l] = t;
-      if (fin_ptr) fin_ptr[l] = step_no;  // Sec. 4.3: last change = finalization
+      if (fin_ptr) fin_ptr[l] = step_no;  // Sec. 5.1: last change = finalization
     }
     if (t == a.mask_id) atomicAdd(&s_nmask_after, 1);
     if (a.flags) a.flags[(size_t)b * Lb + l] = (uint8_t)f;
     if (a.bitmap) a.bitmap[(size_t)b * Lb + l] = t == a.mask_id;
   }
   __syncthreads();
-  const bool adv = !a.standalone && a.advance && s_nmask_after == 0;
-  if (!a.standalone && a.next_verify) {
-    // the next step's Y_cur: this block, or the next one after an advance
-    int nmask = s_nmask_after, nkeep = Lb - s_nmask_after;
-    if (adv) {
-      const int nbs = a.block_start[b] + Lb;
-      if (tid == 0) { s_nmask = 0; s_any_draft = 0; }
-      __syncthreads();
-      if (nbs < a.G) {
-        const int32_t* nxt = a.tokens + (size_t)b * a.S + a.P + (nbs > a.G - Lb ? a.G - Lb : nbs);
-        for (int l = tid; l < Lb; l += 256) {
-          if (nxt[l] == a.mask_id) atomicAdd(&s_nmask, 1);
-          else atomicAdd(&s_any_draft, 1);
-        }
-      }
-      __syncthreads();
-      nmask = s_nmask;
-      nkeep = nbs < a.G ? s_any_draft : 0;
+  if (a.standalone) {
+    if (tid == 0) {
+      if (a.n_masked) a.n_masked[b] = s_nmask_after;
+      if (a.seq_steps) a.seq_steps[b] += 1;
     }
-    if (tid == 0) a.next_verify[b] = nmask > 0 && nkeep > 0;
+    return;
   }
   if (tid == 0) {
     if (a.n_masked) a.n_masked[b] = s_nmask_after;
     if (a.seq_steps) a.seq_steps[b] += 1;
-    if (!a.standalone && a.block_steps) a.block_steps[b] = steps_before + 1;
-    if (adv) {
-      a.block_start[b] += Lb;
-      if (a.block_steps) a.block_steps[b] = 0;
-    }
+    if (a.block_steps) a.block_steps[b] = steps_before + 1;
   }
+  advance_block(a, b, s_nmask_after);
 }
 
-// next_verify[b] for a state before any step: the sequence is active and its
-// Y_cur holds both a mask and a non-mask token.
+// State before the first step of a call.  With advance (decode mode) a
+// sequence whose Y_cur holds no mask first moves to the first later block that
+// holds one, or to G, and its block step count restarts (a resumed or
+// pre-filled state).  Then next_verify[b] = the sequence is active and its
+// Y_cur holds both a mask and a non-mask token.  One wave per sequence.
 __global__ __launch_bounds__(64) void probe_verify_kernel(const StepGeom g,
                                                           const int32_t* __restrict__ tokens,
-                                                          int32_t* __restrict__ next_verify) {
+                                                          int32_t* __restrict__ next_verify,
+                                                          int32_t* block_start, int32_t* block_steps,
+                                                          int advance) {
   const int b = blockIdx.x, lane = threadIdx.x;
-  const int bs = g.block_start[b];
+  int bs = g.block_start[b];
+  const int32_t* resp = tokens + (size_t)b * g.S + g.P;
+  if (advance && bs >= 0 && bs < g.G) {
+    int first = g.G;
+    for (int j = bs + lane; j < g.G; j += 64)
+      if (resp[j] == g.mask_id) { first = j; break; }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) first = min(first, __shfl_xor(first, o, 64));
+    const int nbs = first >= g.G ? g.G : bs + (first - bs) / g.Lb * g.Lb;
+    if (nbs != bs && lane == 0) {
+      block_start[b] = nbs;
+      if (block_steps) block_steps[b] = 0;
+    }
+    bs = nbs;
+  }
   int nmask = 0, nkeep = 0;
   if (bs < g.G) {
-    const int32_t* cur = tokens + (size_t)b * g.S + cur_start(g, b);
+    const int c = bs < 0 ? 0 : (bs > g.G - g.Lb ? g.G - g.Lb : bs);
     for (int l = lane; l < g.Lb; l += 64) {
-      const bool m = cur[l] == g.mask_id;
+      const bool m = resp[c + l] == g.mask_id;
       nmask += m;
       nkeep += !m;
     }
@@ -385,8 +442,9 @@ hipError_t launch_loss_merge(const LmStatsOut& lm, int R, void* out, hipStream_t
 }
 
 hipError_t launch_probe_verify(const StepGeom& g, const int32_t* tokens, int32_t* next_verify,
-                               hipStream_t st) {
-  probe_verify_kernel<<<g.B, 64, 0, st>>>(g, tokens, next_verify);
+                               hipStream_t st, int32_t* block_start, int32_t* block_steps) {
+  probe_verify_kernel<<<g.B, 64, 0, st>>>(g, tokens, next_verify, block_start, block_steps,
+                                          block_start != nullptr);
   return hipGetLastError();
 }
 

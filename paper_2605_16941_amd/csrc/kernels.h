@@ -160,7 +160,7 @@ struct DecideArgs {
   int32_t* tokens; int S, P, G;
   int32_t* block_start;  // [B]
   int32_t* block_steps;  // [B] or null
-  int advance;           // move block_start to the next block when Y_cur is full
+  int advance;           // move block_start to the next block holding a mask when Y_cur is full
   int32_t* seq_steps;    // [B] steps counter or null
   uint8_t* flags;        // [B, Lb] or null
   uint8_t* bitmap;       // [B, Lb] or null (standalone)
@@ -176,13 +176,17 @@ struct DecideArgs {
   int32_t* next_verify;
 };
 hipError_t launch_decide(const DecideArgs& a, hipStream_t st);
-// WINO+ per-row quantities (Sec. 4.3) from LM-head partials of R rows (pz
+// WINO+ per-row quantities (Sec. 5.3) from LM-head partials of R rows (pz
 // required): out[r] = {entropy, nll of the target, greedy confidence, argmax}
 // (wino_loss_row layout).
 hipError_t launch_loss_merge(const LmStatsOut& lm, int R, void* out, hipStream_t st);
 // next_verify[b] as above for the state before any step (fused-step layout).
+// With block_start (the same array as g.block_start, writable), a sequence
+// whose Y_cur holds no mask first moves to the first later block holding one
+// (or to G) and its block_steps entry (if given) restarts at 0.
 hipError_t launch_probe_verify(const StepGeom& g, const int32_t* tokens, int32_t* next_verify,
-                               hipStream_t st);
+                               hipStream_t st, int32_t* block_start = nullptr,
+                               int32_t* block_steps = nullptr);
 
 // Standalone epilogue statistics: for each (b, l) pick the current row
 // (masked) or the shadow row (unmasked) of bf16 logits [B, 2Lb, V], and write

@@ -434,9 +434,10 @@ wino_status wino_create(const wino_model_config* cfg, const wino_weights* w, int
   c->lm_bias = w->lm_bias;
   c->L = make_layout(*cfg, max_batch, max_seq);
 
-  if (hipGetDevice(&c->device) != hipSuccess) { delete c; return WINO_ERR_HIP; }
+  // an optional cap on the workspace (bytes), checked before any HIP call
   const char* lim = std::getenv("WINO_WORKSPACE_LIMIT");
   if (lim && std::strtoull(lim, nullptr, 10) < c->L.total) { delete c; return WINO_ERR_NO_MEMORY; }
+  if (hipGetDevice(&c->device) != hipSuccess) { delete c; return WINO_ERR_HIP; }
   if (hipMalloc(&c->ws, c->L.total) != hipSuccess) { c->ws = nullptr; delete c; return WINO_ERR_NO_MEMORY; }
   if (hipHostMalloc(reinterpret_cast<void**>(&c->h_pinned), sizeof(int32_t) * 4 * max_batch) != hipSuccess) {
     hipFree(c->ws);
@@ -544,20 +545,27 @@ wino_status wino_decode_block(wino_ctx* c, const wino_params* p, int32_t* d_toke
 }
 
 wino_status wino_decode(wino_ctx* c, const wino_params* p, int32_t* d_tokens, int32_t* d_block_start,
-                        int32_t* d_final_step, int32_t* h_steps_per_seq, int32_t* h_forward_passes,
-                        void* stream) {
+                        int32_t* d_block_steps, int32_t* d_final_step, int32_t max_forwards,
+                        int32_t* h_steps_per_seq, int32_t* h_forward_passes, void* stream) {
   if (!c) return WINO_ERR_INVALID_ARG;
   wino_status s = validate_params(c, p);
   if (s != WINO_OK) return s;
-  if (!d_tokens || !d_block_start) return WINO_ERR_INVALID_ARG;
+  if (!d_tokens || !d_block_start || max_forwards < 0) return WINO_ERR_INVALID_ARG;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int B = p->batch;
   const int cap = block_cap(p);
-  const long max_forwards = (long)(p->gen_len / p->block_len) * cap;
-  HIP_TRY(c, hipMemsetAsync(c->block_steps(), 0, sizeof(int32_t) * 2 * c->max_batch, st));
+  // every block takes at most `cap` steps, so this many forwards finish any state
+  const long budget = (long)(p->gen_len / p->block_len) * cap;
+  // block steps: the caller's (a resumed state) or zeros
+  int32_t* bsteps = d_block_steps ? d_block_steps : c->block_steps();
+  if (!d_block_steps)
+    HIP_TRY(c, hipMemsetAsync(c->block_steps(), 0, sizeof(int32_t) * c->max_batch, st));
+  HIP_TRY(c, hipMemsetAsync(c->seq_steps(), 0, sizeof(int32_t) * c->max_batch, st));
   int forwards = 0;
   int32_t* h_nv = c->h_pinned + 2 * B;  // next_verify per sequence
-  HIP_TRY(c, launch_probe_verify(make_geom(p, d_block_start), d_tokens, c->next_verify(), st));
+  // blocks holding no mask at the start (a resumed or pre-filled state) are skipped
+  HIP_TRY(c, launch_probe_verify(make_geom(p, d_block_start), d_tokens, c->next_verify(), st,
+                                 d_block_start, bsteps));
   HIP_TRY(c, hipMemcpyAsync(h_nv, c->next_verify(), sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
   HIP_TRY(c, hipMemcpyAsync(c->h_pinned, d_block_start, sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
   HIP_TRY(c, hipStreamSynchronize(st));
@@ -565,17 +573,17 @@ wino_status wino_decode(wino_ctx* c, const wino_params* p, int32_t* d_tokens, in
     bool all_done = true;
     for (int b = 0; b < B; ++b) all_done &= c->h_pinned[b] >= p->gen_len;
     if (all_done) break;
-    if (forwards >= max_forwards) {
+    if (max_forwards > 0 && forwards >= max_forwards) break;  // a resumable checkpoint
+    if (forwards >= budget) {
       c->err = "decode exceeded its forward budget (a block hit its step cap)";
       return WINO_ERR_STEP_CAP;
     }
-    s = step_impl(c, p, d_tokens, d_block_start, c->block_steps(), nullptr, c->n_masked(), nullptr, 1,
+    s = step_impl(c, p, d_tokens, d_block_start, bsteps, nullptr, c->n_masked(), nullptr, 1,
                   c->seq_steps(), need_shadow(p, h_nv), st, d_final_step);
     if (s != WINO_OK) return s;
     ++forwards;
     HIP_TRY(c, hipMemcpyAsync(c->h_pinned, d_block_start, sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
-    HIP_TRY(c, hipMemcpyAsync(c->h_pinned + B, c->block_steps(), sizeof(int32_t) * B,
-                              hipMemcpyDeviceToHost, st));
+    HIP_TRY(c, hipMemcpyAsync(c->h_pinned + B, bsteps, sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
     HIP_TRY(c, hipMemcpyAsync(h_nv, c->next_verify(), sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
     HIP_TRY(c, hipStreamSynchronize(st));
     if ((p->flags & WINO_FLAG_NO_CAP_FILL) && p->tokens_per_step == 0)

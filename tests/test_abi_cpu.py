@@ -86,7 +86,7 @@ def test_create_rejects_bad_arguments_before_gpu_work(abi):
 def test_entry_points_reject_null_context_and_bad_params(abi):
     p = abi.make_params(1, 32, 64, 16, 4095)
     assert abi.lib.wino_step(None, C.byref(p), None, None, None, None, None, None, None) == -1
-    assert abi.lib.wino_decode(None, C.byref(p), None, None, None, None, None, None) == -1
+    assert abi.lib.wino_decode(None, C.byref(p), None, None, None, None, 0, None, None, None) == -1
     assert abi.lib.wino_decode_block(None, C.byref(p), None, None, None, None, None) == -1
     assert abi.lib.wino_destroy(None) == -1
     assert abi.lib.wino_profile(None, 1) == -1
@@ -100,3 +100,35 @@ def test_entry_points_reject_null_context_and_bad_params(abi):
     assert abi.lib.wino_epilogue(C.byref(ok), 4100, ws, ws, ws, None, None, ws, 1 << 20, None) == -2
     assert abi.lib.wino_epilogue(C.byref(ok), 4096, ws, ws, ws, None, None, ws, 16, None) == -2
     assert abi.lib.wino_epilogue(C.byref(ok), 4096, None, ws, ws, None, None, ws, 1 << 20, None) == -1
+
+
+def fake_weights(abi, n_layers):
+    """A weights struct of non-null placeholder pointers: wino_create stores
+    them and never dereferences them before its workspace check."""
+    keep = []
+
+    def arr():
+        a = (C.c_void_p * n_layers)(*([0x1000] * n_layers))
+        keep.append(a)
+        return a
+
+    w = abi.wino_weights(0x1000, arr(), arr(), arr(), arr(), arr(), arr(), 0x1000, 0x1000, None)
+    return w, keep
+
+
+def test_workspace_limit_is_enforced_before_any_hip_call(abi, monkeypatch):
+    """WINO_WORKSPACE_LIMIT (bytes) below what the context needs makes
+    wino_create return WINO_ERR_NO_MEMORY before it touches the HIP runtime,
+    so the out-of-memory path is exercised without a GPU."""
+    cfg = tiny_cfg(abi)
+    need = abi.wino_workspace_bytes(cfg, 2, 112)
+    w, keep = fake_weights(abi, cfg.n_layers)
+    out = C.c_void_p()
+    for limit in (0, need // 2, need - 1):
+        monkeypatch.setenv("WINO_WORKSPACE_LIMIT", str(limit))
+        assert abi.lib.wino_create(C.byref(cfg), C.byref(w), 2, 112, C.byref(out)) == -4
+        assert out.value is None
+    # a larger batch needs more than a limit sized for batch 2
+    monkeypatch.setenv("WINO_WORKSPACE_LIMIT", str(need))
+    assert abi.lib.wino_create(C.byref(cfg), C.byref(w), 3, 112, C.byref(out)) == -4
+

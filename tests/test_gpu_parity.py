@@ -1,103 +1,31 @@
-"""Parity of the HIP path (through the C ABI) against the float64 oracle.
+"""Parity of the HIP path (through the C ABI) against the float64 oracle:
+forward pieces (embedding, residual stream per sublayer, logits), the block
+and baseline decoders, the step cap, the WINO+ per-row quantities, argument
+checks, determinism and the GEMM tiles.
 
 Every input is seeded and synthetic; oracle inputs are the same bytes the GPU
-receives.  Tolerances: logits within 2e-2 max relative error per row against
-the float64 oracle.  Decisions and token ids are floating-point-decided
-integers, so both sides take them in the kernel's precision: the oracle runs
-with bf16 rounding at the points where the kernels materialise bf16
-activations (everything else float64), and decisions must be bit-exact
-wherever that oracle's deciding probability is more than 1e-3 from its
-threshold (ids also need a top-2 gap above 1e-3).  The probability gap to the
-float64 oracle is asserted separately.
+receives.  Logits must lie within 2e-2 max relative error per row of the
+float64 oracle.  Decisions are judged by the float64 oracle (see
+test_gpu_decisions.py for the contract tests); the oracle with bf16 rounding
+at the kernels' rounding points serves only to size the tolerance of the
+residual-stream checks (how far float32-level noise moves a bf16 pipeline).
 """
-import math
-
 import numpy as np
 import pytest
 import torch
 
 import wino_inputs as wi
-from oracle import epilogue as E
 from oracle import model as M
 from oracle import wino as W
-from helpers import (LOGIT_TOL, MARGIN, decided_mask, forced_is_robust, rowwise_rel_err, to_cpu,
-                     to_device)
+from helpers import (LOGIT_TOL, RANK_GAP, batch_tokens, decided_mask, decode_prefix_compare, forced_is_robust, fp64_provider,
+                     gpu_step, oracle_params, oracle_trajectory, rowwise_rel_err, tiny, to_cpu, to_device)
 
 pytestmark = pytest.mark.gpu
-
-STATS_DT = np.dtype([("m_all", "<f4"), ("sumexp", "<f4"), ("z_best", "<f4"), ("z_target", "<f4"),
-                     ("argmax", "<i4"), ("row_kind", "<i4")])
-
 
 @pytest.fixture(scope="module")
 def P():
     import paper_2605_16941_amd as pkg
     return pkg
-
-
-def tiny(variant="wide", seed=0, gain_std=0.1, **kw):
-    cfg = wi.preset("tiny", **kw)
-    lhs = wi.wide_lm_head_std(cfg) if variant == "wide" else None
-    return cfg, wi.model_weights(cfg, seed=seed, lm_head_std=lhs, gain_std=gain_std)
-
-
-def batch_tokens(cfg, B, p, g, seed=0, fill=None):
-    pr = wi.prompts(cfg, B, p, seed=seed)
-    tok = wi.initial_tokens(pr, g, cfg.mask_id).numpy().astype(np.int64)
-    if fill:
-        rng = np.random.default_rng(seed)
-        for b in range(B):
-            for (lo, hi, frac) in fill:
-                idx = np.arange(p + lo, p + hi)
-                sel = idx[rng.random(len(idx)) < frac]
-                tok[b, sel] = rng.integers(0, cfg.mask_id, len(sel))
-    return tok
-
-
-def gpu_step(P, model, prm, tokens, block_start, block_steps):
-    B, lb = tokens.shape[0], prm.block_len
-    tok = torch.tensor(tokens, dtype=torch.int32, device="cuda")
-    bs = torch.tensor(block_start, dtype=torch.int32, device="cuda")
-    st = torch.tensor(block_steps, dtype=torch.int32, device="cuda")
-    flags = torch.full((B, lb), 255, dtype=torch.uint8, device="cuda")
-    nm = torch.full((B,), -7, dtype=torch.int32, device="cuda")
-    stats = torch.zeros(B * lb * STATS_DT.itemsize, dtype=torch.uint8, device="cuda")
-    P.wino_step(model.ctx, prm, tok, bs, st, flags, nm, stats)
-    torch.cuda.synchronize()
-    return (tok.cpu().numpy(), flags.cpu().numpy(), nm.cpu().numpy(), st.cpu().numpy(),
-            stats.cpu().numpy().view(STATS_DT).reshape(B, lb))
-
-
-def oracle_params(prm_c, **kw):
-    return W.Params(prm_c.prompt_len, prm_c.gen_len, prm_c.block_len, prm_c.mask_id,
-                    float(np.float32(prm_c.tau1)), float(np.float32(prm_c.tau2)), prm_c.max_steps, **kw)
-
-
-def compare_step(gpu_tok, gpu_flags, r, cur, mask_id, tau1, c0, lb, label="", margin=MARGIN):
-    """Assert GPU decisions equal the oracle's where the oracle fixes them:
-    deciding probability more than `margin` from its threshold (and top-2 gap
-    above `margin` for drafted ids).  Returns how many positions were compared."""
-    masked = cur == mask_id
-    ok = (r.margin > margin) & ~(masked & (r.top2_gap <= margin))
-    cap_now = np.any(r.flags == W.CAPFILL)
-    if cap_now:
-        ok = ~masked | (r.top2_gap > margin)
-    else:
-        confm = r.conf[masked]
-        if masked.any() and not np.any(confm > tau1 + margin):
-            c = np.sort(confm)
-            if np.all(confm < tau1 - margin) and (len(c) < 2 or c[-1] - c[-2] > margin):
-                pass  # the forced draft is fixed: compare it
-            else:
-                ok &= ~masked
-    n = 0
-    for l in range(lb):
-        if not ok[l]:
-            continue
-        assert gpu_flags[l] == r.flags[l], f"{label} pos {l}: flag {gpu_flags[l]} != {r.flags[l]}"
-        assert gpu_tok[c0 + l] == r.tokens[c0 + l], f"{label} pos {l}: token differs"
-        n += 1
-    return n
 
 
 # ---------------------------------------------------------------- forward pieces
@@ -196,22 +124,14 @@ def test_ragged_shapes_forward_and_decode(P, p, g, lb, B):
         errs16.append(rowwise_rel_err(got[b], ref16))
     print(f"T={T}: vs bf16-point {max(errs16):.2e}, oracle self-sensitivity {chaos:.2e}")
     assert max(errs16) < 3 * chaos + 1e-4
-    # decode from all-mask responses with the same prompts
+    # decode from all-mask responses with the same prompts, one forward per
+    # call, against the float64 oracle up to its first non-robust step
     tok0 = tok.copy()
     tok0[:, p:] = cfg.mask_id
-    dt = torch.tensor(tok0, dtype=torch.int32, device="cuda")
-    bs = torch.zeros(B, dtype=torch.int32, device="cuda")
-    steps, forwards = P.wino_decode(model.ctx, prm, dt, bs)
-    torch.cuda.synchronize()
-    dgot = dt.cpu().numpy()
-    assert not np.any(dgot[:, p:] == cfg.mask_id) and np.array_equal(dgot[:, :p], tok0[:, :p])
-    oprm = oracle_params(prm)
-    prov = W.ModelProvider(w, cfg, act_round=M.round_bf16)
-    for b in range(B):
-        traj, final = oracle_trajectory(prov, tok0[b], oprm)
-        if robust_trajectory(traj, p, lb, cfg.mask_id):
-            assert np.array_equal(dgot[b], final), f"seq {b}: decode differs from the oracle"
-            assert steps[b] == len(traj)
+    compared, diverged, forwards, trajs = decode_prefix_compare(P, model, prm, oracle_params(prm),
+                                                                fp64_provider(w, cfg), tok0, f"T={T}")
+    print(f"T={T}: decode steps compared {compared} of {[len(t) for t in trajs]}, divergence {diverged}")
+    assert sum(compared) >= 1
     model.close()
 
 
@@ -285,109 +205,7 @@ def test_logits_match_oracle(P, variant):
     model.close()
 
 
-# ---------------------------------------------------------------- one step, teacher forced
-def oracle_trajectory(prov, tokens0, prm):
-    """[(tokens before, block_start, block_steps, StepResult)] of a full decode."""
-    out = []
-    tok = np.asarray(tokens0, dtype=np.int64).copy()
-    for blk in range(prm.gen_len // prm.block_len):
-        bs, steps = blk * prm.block_len, 0
-        c0 = prm.prompt_len + bs
-        while True:
-            r = W.step(prov, tok, prm, bs, steps)
-            out.append((tok.copy(), bs, steps, r))
-            tok = r.tokens
-            steps += 1
-            if not np.any(tok[c0:c0 + prm.block_len] == prm.mask_id):
-                break
-    return out, tok
-
-
-@pytest.mark.parametrize("variant,tau1,tau2", [("wide", 0.7, 0.9), ("wide", 0.5, 0.9),
-                                               ("literal", 0.7, 0.9), ("wide", 0.95, 0.0)])
-def test_teacher_forced_steps(P, variant, tau1, tau2):
-    cfg, w = tiny(variant, seed=1)
-    wd = to_device(w)
-    p, g, lb = 32, 64, 16
-    model = P.WinoModel(cfg, wd, 2, p + g + lb)
-    prm_c = P.make_params(2, p, g, lb, cfg.mask_id, tau1, tau2)
-    prm = oracle_params(prm_c)
-    tok0 = batch_tokens(cfg, 2, p, g, seed=5)
-    prov = W.ModelProvider(w, cfg, act_round=M.round_bf16)
-    prov64 = W.ModelProvider(w, cfg)
-    trajs = [oracle_trajectory(prov, tok0[b], prm)[0] for b in range(2)]
-    n_cmp = 0
-    for k in range(max(len(t) for t in trajs)):
-        states = [t[min(k, len(t) - 1)] for t in trajs]
-        tokens = np.stack([s[0] for s in states])
-        gt, gf, gnm, gst, gstats = gpu_step(P, model, prm_c, tokens, [s[1] for s in states],
-                                            [s[2] for s in states])
-        for b, (tb, bs, steps, r) in enumerate(states):
-            c0 = p + bs
-            cur = tb[c0:c0 + lb]
-            n_cmp += compare_step(gt[b], gf[b], r, cur, cfg.mask_id, prm.tau1, c0, lb, f"step {k} seq {b}")
-            # nothing outside the current block may change
-            outside = np.ones(p + g, bool)
-            outside[c0:c0 + lb] = False
-            assert np.array_equal(gt[b][outside], tb[outside])
-            assert gst[b] == steps + 1
-            assert gnm[b] == np.sum(gt[b][c0:c0 + lb] == cfg.mask_id)
-            # the probability behind each decision, within bf16-pipeline accuracy;
-            # with tau2 <= 0 nothing can be re-masked, the step runs without the
-            # shadow block and unmasked positions report no verification
-            masked = cur == cfg.mask_id
-            verified = ~masked if tau2 > 0 else np.zeros_like(masked)
-            read = masked | verified
-            val = np.exp(np.where(masked, gstats["z_best"][b], gstats["z_target"][b]) - gstats["m_all"][b]) / gstats["sumexp"][b]
-            ref = np.where(masked, r.conf, r.s)
-            assert np.max(np.abs(val - ref)[read]) < 5e-3
-            r64 = W.step(prov64, tb, prm, bs, steps)
-            assert np.max(np.abs(val - np.where(masked, r64.conf, r64.s))[read]) < 2e-2
-            assert np.array_equal(gstats["row_kind"][b], np.where(masked, 0, np.where(verified, 1, 2)))
-    assert n_cmp > 0
-    model.close()
-
-
-# ---------------------------------------------------------------- free-running decode
-@pytest.mark.parametrize("variant,tau1,tau2,lb", [("wide", 0.7, 0.9, 16), ("literal", 0.7, 0.9, 16),
-                                                  ("wide", 0.6, 0.9, 64), ("wide", 0.8, 0.95, 8),
-                                                  ("wide", 0.9, 0.0, 16), ("wide", 0.7, 0.9, 1),
-                                                  ("wide", 1.0, 0.0, 16)])
-def test_decode_matches_oracle(P, variant, tau1, tau2, lb):
-    cfg, w = tiny(variant, seed=2)
-    wd = to_device(w)
-    p, g, B = 32, 64, 2
-    model = P.WinoModel(cfg, wd, B, p + g + lb)
-    prm_c = P.make_params(B, p, g, lb, cfg.mask_id, tau1, tau2)
-    prm = oracle_params(prm_c)
-    tok0 = batch_tokens(cfg, B, p, g, seed=9)
-    tok = torch.tensor(tok0, dtype=torch.int32, device="cuda")
-    bs = torch.zeros(B, dtype=torch.int32, device="cuda")
-    fin = torch.zeros(B, g, dtype=torch.int32, device="cuda")
-    steps, forwards = P.wino_decode(model.ctx, prm_c, tok, bs, fin)
-    torch.cuda.synchronize()
-    got = tok.cpu().numpy()
-    fin = fin.cpu().numpy()
-    assert np.all(bs.cpu().numpy() == g)
-    assert not np.any(got[:, p:] == cfg.mask_id)
-    assert np.array_equal(got[:, :p], tok0[:, :p])
-    assert forwards == max(steps)
-    for b in range(B):
-        traj, final = oracle_trajectory(W.ModelProvider(w, cfg, act_round=M.round_bf16), tok0[b], prm)
-        robust = all(np.all(decided_mask(r.margin, r.top2_gap, t[c0:c0 + lb] == cfg.mask_id))
-                     and (not np.any(r.flags == W.FORCED)
-                          or forced_is_robust(r.conf, t[c0:c0 + lb] == cfg.mask_id))
-                     for (t, bs_, _, r) in traj for c0 in [p + bs_])
-        if robust:
-            assert np.array_equal(got[b], final), f"seq {b}: decoded tokens differ"
-            assert steps[b] == len(traj)
-            # Sec. 4.3 finalization steps, from the oracle's states Y^(0..K)
-            t = W.finalization_steps([tok0[b]] + [r.tokens for (_, _, _, r) in traj], p)
-            assert np.array_equal(fin[b], t[p:]), f"seq {b}: finalization steps differ"
-        assert np.all((fin[b] >= 1) & (fin[b] <= steps[b]))
-    model.close()
-
-
+# ---------------------------------------------------------------- block and baseline decoders
 def test_decode_block_and_idle_sequences(P):
     cfg, w = tiny("wide", seed=4)
     wd = to_device(w)
@@ -451,7 +269,7 @@ def test_decode_block_matches_oracle(P, mixed):
     torch.cuda.synchronize()
     got = tok.cpu().numpy()
     fin = fin.cpu().numpy()
-    prov = W.ModelProvider(w, cfg, act_round=M.round_bf16)
+    prov = fp64_provider(w, cfg)
     n_cmp = 0
     for b in range(B):
         traj, final = block_trajectory(prov, tok0[b], prm, starts[b])
@@ -463,7 +281,7 @@ def test_decode_block_matches_oracle(P, mixed):
         if robust_trajectory(traj, p, lb, cfg.mask_id):
             assert np.array_equal(got[b], final), f"seq {b}: block differs from the oracle"
             assert steps[b] == len(traj)
-            # Sec. 4.3 finalization steps relative to this call (0: never changed,
+            # Sec. 5.1 finalization steps relative to this call (0: never changed,
             # e.g. a kept pre-filled draft); re-masked drafts finalise later
             t = W.finalization_steps([tok0[b]] + [r.tokens for (_, _, _, r) in traj], p)
             assert np.array_equal(fin[b], t[p:]), f"seq {b}: finalization steps differ"
@@ -481,9 +299,10 @@ def test_baseline_decoders_match_oracle(P, m):
     the oracle's m-th / (m+1)-th gap is robust; everywhere else the GPU's
     choice must be a valid top-m set: no undrafted mask more confident than a
     drafted one by more than the tolerance.  A rank or an id compares two
-    probabilities, each within 5e-3 of the kernel-precision oracle (the bound
-    test_teacher_forced_steps holds), so both are fixed only by gaps > 1e-2."""
-    tol = 1e-2
+    probabilities, each within PROB_ERR of the float64 oracle (the bound the
+    contract tests hold on this model), so both are fixed only by gaps above
+    RANK_GAP = 2 * PROB_ERR."""
+    tol = RANK_GAP
     cfg, w = tiny("wide", seed=4)
     wd = to_device(w)
     p, g, lb, B = 32, 64, 16, 2
@@ -491,7 +310,7 @@ def test_baseline_decoders_match_oracle(P, m):
     prm_c = P.make_params(B, p, g, lb, cfg.mask_id, tokens_per_step=m)
     prm = oracle_params(prm_c, tokens_per_step=m)
     tok0 = batch_tokens(cfg, B, p, g, seed=9)
-    prov = W.ModelProvider(w, cfg, act_round=M.round_bf16)
+    prov = fp64_provider(w, cfg)
     trajs = [oracle_trajectory(prov, tok0[b], prm)[0] for b in range(B)]
     n_exact = 0
     for k in range(max(len(t) for t in trajs)):
@@ -531,7 +350,7 @@ def test_baseline_decoders_match_oracle(P, m):
 
 @pytest.mark.parametrize("tau1,m", [(1.0, 1), (-1.0, 16)])
 def test_threshold_special_cases_equal_baselines(P, tau1, m):
-    """Sec. 5 special cases on the same kernels: with tau2 = 0 nothing is
+    """Special cases on the same kernels (the tau2 = 0 ablation of Sec. 6.3): with tau2 = 0 nothing is
     re-masked; tau1 >= 1 then drafts only the forced top-1 position (Eq. 2 can
     never exceed 1), which is Eq. 1 greedy decoding, one token per step; tau1 < 0
     drafts every masked position at once, one step per block.  Both must equal
@@ -564,7 +383,7 @@ LOSS_DT = np.dtype([("entropy", "<f4"), ("nll", "<f4"), ("conf", "<f4"), ("argma
 
 @pytest.mark.parametrize("variant", ["literal", "wide"])
 def test_row_losses_match_oracle(P, variant):
-    """WINO+ per-row quantities (Sec. 4.3) of training states: entropy, target
+    """WINO+ per-row quantities (Sec. 5.3) of training states (Sec. 5.2): entropy, target
     NLL and greedy prediction of every response row, fused into the LM head.
     Two sequences whose training states reveal the tokens finalized before
     different steps; 128 response rows in chunks of the workspace's rows."""
@@ -592,7 +411,7 @@ def test_row_losses_match_oracle(P, variant):
             assert np.max(np.abs(got[b]["entropy"] - e)) < 2 * tol
             assert np.max(np.abs(got[b]["nll"] - nll) / (1 + nll)) < 2 * tol
             assert np.max(np.abs(got[b]["conf"] - conf)) < tol
-            if act_round is not None:
+            if act_round is None:
                 pr = W.softmax_rows(z)
                 pr[:, cfg.mask_id] = -1.0
                 top = np.sort(pr, axis=-1)
@@ -632,7 +451,7 @@ def test_step_cap_without_forced_draft(P, cap_fill):
     got = tok.cpu().numpy()
     assert not np.any(got[:, p:] == cfg.mask_id)
     prm = oracle_params(prm_c, force_top1=False, cap_fill=True)
-    prov = W.ModelProvider(w, cfg, act_round=M.round_bf16)
+    prov = fp64_provider(w, cfg)
     compared = 0
     for b in range(B):
         traj, final = oracle_trajectory(prov, tok0[b], prm)
@@ -728,133 +547,10 @@ def test_gemm_tiles_within_exact_product_bound(P, M, N, K, monkeypatch):
     assert torch.equal(outs[6], outs[11]) and torch.equal(outs[9], outs[12])
 
 
-# ---------------------------------------------------------------- standalone epilogue
-@pytest.mark.parametrize("B,lb,V,heights", [(2, 8, 4096, (10.0, 16.0)), (8, 32, 126464, (10.0, 16.0)),
-                                            (8, 32, 126464, (0.0, 12.0)), (3, 5, 1000, (0.0, 14.0))])
-def test_epilogue_matches_oracle(P, B, lb, V, heights):
-    mask = V - 1 if V != 126464 else 126463
-    logits, cur, _ = wi.epilogue_inputs(B, lb, V, mask, seed=2, heights=heights, device="cuda")
-    cur0 = cur.cpu().numpy()
-    prm = P.make_params(B, 1, lb, lb, mask, 0.7, 0.9)
-    ws = torch.empty(P.wino_epilogue_workspace_bytes(B, lb, V), dtype=torch.uint8, device="cuda")
-    bitmap = torch.full((B, lb), 9, dtype=torch.uint8, device="cuda")
-    flags = torch.full((B, lb), 9, dtype=torch.uint8, device="cuda")
-    stats = torch.zeros(B * lb * STATS_DT.itemsize, dtype=torch.uint8, device="cuda")
-    P.wino_epilogue(prm, V, logits, cur, bitmap, flags, stats, ws)
-    torch.cuda.synchronize()
-    ref = E.decide(logits.cpu(), cur0, mask, float(np.float32(0.7)), float(np.float32(0.9)))
-    gt, gb, gf = cur.cpu().numpy(), bitmap.cpu().numpy(), flags.cpu().numpy()
-    st = stats.cpu().numpy().view(STATS_DT).reshape(B, lb)
-    z = logits.cpu().double().numpy()
-    for b in range(B):
-        masked = cur0[b] == mask
-        rows = np.where(masked, np.arange(lb), lb + np.arange(lb))
-        zr = z[b, rows]
-        # exact statistics: bf16 inputs are exact in fp32
-        assert np.array_equal(st["m_all"][b], zr.max(-1).astype(np.float32))
-        np.testing.assert_allclose(st["sumexp"][b], np.exp(zr - zr.max(-1, keepdims=True)).sum(-1), rtol=1e-5)
-        zx = zr.copy()
-        zx[:, mask] = -np.inf
-        assert np.array_equal(st["argmax"][b], zx.argmax(-1))
-        ok = decided_mask(ref["margin"][b], ref["gap"][b], masked)
-        if masked.any() and not np.any(ref["conf"][b][masked] > 0.7 + MARGIN):
-            ok &= ~masked
-        assert np.array_equal(gf[b][ok], ref["flags"][b][ok])
-        assert np.array_equal(gt[b][ok], ref["tokens"][b][ok])
-        assert np.array_equal(gb[b][ok], ref["bitmap"][b][ok])
 
 
-# ---------------------------------------------------------------- full-size shapes, one layer
 def big_one_layer(name, seed=0, wide=True):
     cfg = wi.preset(name, n_layers=1)
     lhs = wi.wide_lm_head_std(cfg) if wide else None
     w = wi.model_weights(cfg, seed=seed, device="cuda", lm_head_std=lhs, gain_std=0.1)
     return cfg, w
-
-
-@pytest.mark.slow
-@pytest.mark.parametrize("name,B,p,g,lb,check,image", [("llada8b", 1, 256, 256, 32, [0], 0),
-                                                       ("llada8b", 16, 256, 256, 32, [0, 11], 0),
-                                                       ("mmada8b", 4, 1024, 1024, 64, [2], 576)])
-def test_full_shape_one_layer_step(P, name, B, p, g, lb, check, image):
-    cfg, wd = big_one_layer(name)
-    model = P.WinoModel(cfg, wd, B, p + g + lb)
-    tau1 = 0.6 if name == "mmada8b" else 0.7
-    prm_c = P.make_params(B, p, g, lb, cfg.mask_id, tau1, 0.9)
-    prm = oracle_params(prm_c)
-    pr = wi.prompts(cfg, B, p, seed=1, image_prefix=image).numpy()
-    tok0 = np.concatenate([pr, np.full((B, g), cfg.mask_id)], axis=1).astype(np.int64)
-    rng = np.random.default_rng(0)
-    bstart = [lb * (b % (g // lb)) for b in range(B)]
-    for b in range(B):   # earlier blocks decoded; current block partly drafted
-        tok0[b, p:p + bstart[b]] = rng.integers(0, cfg.mask_id, bstart[b])
-        c0 = p + bstart[b]
-        sel = np.arange(c0, c0 + lb)[rng.random(lb) < 0.5]
-        tok0[b, sel] = rng.integers(0, cfg.mask_id, len(sel))
-    gt, gf, gnm, gst, gstats = gpu_step(P, model, prm_c, tok0, bstart, [1] * B)
-    logits = torch.empty(B, 2 * lb, cfg.vocab, dtype=torch.float32, device="cuda")
-    P.wino_debug_logits(model.ctx, prm_c, torch.tensor(tok0, dtype=torch.int32, device="cuda"),
-                        torch.tensor(bstart, dtype=torch.int32, device="cuda"), logits)
-    torch.cuda.synchronize()
-    w = to_cpu(wd)
-    model.close()
-    del wd
-    for b in check:
-        r64 = W.step(W.ModelProvider(w, cfg), tok0[b], prm, bstart[b], 1)
-        r16 = W.step(W.ModelProvider(w, cfg, act_round=M.round_bf16), tok0[b], prm, bstart[b], 1)
-        check_full_step(b, gt, gf, gstats, logits[b].cpu().numpy(), r64, r16, tok0[b], p, lb, cfg, prm,
-                        bstart[b])
-
-
-def check_full_step(b, gt, gf, gstats, logits_b, r64, r16, tok_b, p, lb, cfg, prm, bstart_b):
-    """Decisions at the full shape.  delta = the largest gap, over the block,
-    between the float64 oracle's deciding probability and the same oracle run
-    at the kernel's bf16 rounding points (oracle data only): the precision the
-    kernel's arithmetic has.  Decisions must match wherever the float64
-    margin exceeds max(1e-3, 2*delta); the GPU's probabilities must be within
-    3*delta (+1e-4) of float64."""
-    c0 = p + bstart_b
-    cur = tok_b[c0:c0 + lb]
-    masked = cur == cfg.mask_id
-    err = rowwise_rel_err(logits_b, np.concatenate([r64.z_cur, r64.z_shad]))
-    assert err < LOGIT_TOL, f"seq {b}: logits rel err {err}"
-    p64 = np.where(masked, r64.conf, r64.s)
-    delta = float(np.max(np.abs(p64 - np.where(masked, r16.conf, r16.s))))
-    val = np.exp(np.where(masked, gstats["z_best"][b], gstats["z_target"][b]) - gstats["m_all"][b]) / gstats["sumexp"][b]
-    dp64 = float(np.max(np.abs(val - p64)))
-    margin = max(MARGIN, 2 * delta)
-    n = compare_step(gt[b], gf[b], r64, cur, cfg.mask_id, prm.tau1, c0, lb, f"seq {b}", margin=margin)
-    print(f"seq {b}: logits err {err:.2e}; kernel-precision delta {delta:.2e}; GPU |dp| vs fp64 {dp64:.2e}; "
-          f"{n}/{lb} decisions compared at margin {margin:.2e}")
-    assert dp64 <= 3 * delta + 1e-4
-    assert n > 0
-
-
-@pytest.mark.slow
-def test_full_model_step_bs1_literal(P):
-    """All 32 layers at the 8B shape, batch 1, literal init (the benchmark's
-    bs1 configuration); the oracle runs the whole step for the sequence."""
-    cfg = wi.preset("llada8b")
-    wd = wi.model_weights(cfg, seed=0, device="cuda")
-    B, p, g, lb = 1, 256, 256, 32
-    model = P.WinoModel(cfg, wd, B, p + g + lb)
-    prm_c = P.make_params(B, p, g, lb, cfg.mask_id, 0.7, 0.9)
-    prm = oracle_params(prm_c)
-    pr = wi.prompts(cfg, B, p, seed=1000).numpy()
-    tok0 = np.concatenate([pr, np.full((B, g), cfg.mask_id)], axis=1).astype(np.int64)
-    rng = np.random.default_rng(3)
-    tok0[0, p:p + lb] = rng.integers(0, cfg.mask_id, lb)
-    sel = np.arange(p + lb, p + 2 * lb)[rng.random(lb) < 0.5]
-    tok0[0, sel] = rng.integers(0, cfg.mask_id, len(sel))
-    gt, gf, gnm, gst, gstats = gpu_step(P, model, prm_c, tok0, [lb], [1])
-    logits = torch.empty(B, 2 * lb, cfg.vocab, dtype=torch.float32, device="cuda")
-    P.wino_debug_logits(model.ctx, prm_c, torch.tensor(tok0, dtype=torch.int32, device="cuda"),
-                        torch.tensor([lb], dtype=torch.int32, device="cuda"), logits)
-    torch.cuda.synchronize()
-    model.close()
-    w = to_cpu(wd)
-    del wd
-    torch.cuda.empty_cache()
-    r64 = W.step(W.ModelProvider(w, cfg), tok0[0], prm, lb, 1)
-    r16 = W.step(W.ModelProvider(w, cfg, act_round=M.round_bf16), tok0[0], prm, lb, 1)
-    check_full_step(0, gt, gf, gstats, logits[0].cpu().numpy(), r64, r16, tok0[0], p, lb, cfg, prm, lb)

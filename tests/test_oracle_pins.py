@@ -521,7 +521,7 @@ def test_norm_gain_scales_like_the_following_matrix(norm, mat):
     assert np.max(np.abs(h_gain - base)) > 1e-4
 
 
-# ---------------------------------------------------------------- WINO+ per-row quantities (Sec. 4.3)
+# ---------------------------------------------------------------- WINO+ per-row quantities (Sec. 5.3)
 from oracle import losses as L  # noqa: E402
 
 
