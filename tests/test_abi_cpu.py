@@ -132,3 +132,57 @@ def test_workspace_limit_is_enforced_before_any_hip_call(abi, monkeypatch):
     monkeypatch.setenv("WINO_WORKSPACE_LIMIT", str(need))
     assert abi.lib.wino_create(C.byref(cfg), C.byref(w), 3, 112, C.byref(out)) == -4
 
+
+
+SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined"]
+
+
+def _hipcc():
+    for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc"):
+        if cand and os.path.exists(cand):
+            return cand
+    pytest.skip("hipcc not available")
+
+
+def test_host_code_under_address_and_undefined_behaviour_sanitizers():
+    """The library's host code (argument validation, sizing, the GEMM tile
+    planner's rejections, the workspace limit, status strings) built with
+    AddressSanitizer and UndefinedBehaviorSanitizer on the host pass only,
+    linked with tests/host_checks.cpp and run without a GPU: every check
+    passes and no sanitizer reports anything."""
+    import subprocess
+    hipcc = _hipcc()
+    csrc = os.path.join(ROOT, "paper_2605_16941_amd", "csrc")
+    out = os.path.join(ROOT, "_build", "host_sanitize")
+    os.makedirs(out, exist_ok=True)
+    flags = ["-x", "hip", "--offload-arch=gfx950", "-O1", "-g", "-fno-omit-frame-pointer", "-std=c++17",
+             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", *SANITIZE,
+             "-I", os.path.join(ROOT, "include"), "-I", csrc]
+    headers = [os.path.join(ROOT, "include", "wino.h")] + [os.path.join(csrc, h) for h in ("common.h", "kernels.h")]
+    newest_header = max(os.path.getmtime(h) for h in headers)
+    procs, objs = [], []
+    for src in ("k_norm.hip", "k_gemm.hip", "k_attn.hip", "k_decide.hip", "wino.cpp"):
+        path = os.path.join(csrc, src)
+        obj = os.path.join(out, os.path.splitext(src)[0] + ".o")
+        objs.append(obj)
+        if os.path.exists(obj) and os.path.getmtime(obj) > max(os.path.getmtime(path), newest_header):
+            continue
+        procs.append(subprocess.Popen([hipcc, *flags, "-c", path, "-o", obj], stdout=subprocess.PIPE,
+                                      stderr=subprocess.STDOUT, text=True))
+    for p in procs:
+        log = p.communicate()[0]
+        assert p.returncode == 0, log
+    exe = os.path.join(out, "host_checks")
+    drv = os.path.join(ROOT, "tests", "host_checks.cpp")
+    r = subprocess.run([hipcc, "-x", "c++", "-O1", "-g", "-std=c++17", *SANITIZE, "-I", os.path.join(ROOT, "include"),
+                        "-c", drv, "-o", exe + ".o"], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([hipcc, "--offload-arch=gfx950", *SANITIZE, *objs, exe + ".o", "-o", exe],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=0",
+               UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
+    env.pop("WINO_WORKSPACE_LIMIT", None)
+    r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=120)
+    assert r.returncode == 0 and "host checks ok" in r.stdout, r.stdout + r.stderr
+    assert "runtime error" not in r.stderr and "AddressSanitizer" not in r.stderr, r.stderr
