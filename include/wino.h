@@ -220,6 +220,22 @@ wino_status wino_epilogue(const wino_params* p, int32_t vocab, const void* d_log
                           wino_row_stats* d_stats, void* d_workspace, size_t workspace_bytes,
                           void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation):
+ * wino_epilogue without a workspace argument.  Same arguments, kernels and
+ * results as wino_epilogue; its partial statistics live in a library-owned
+ * device array of WINO_EPILOGUE_NOALLOC_MAX_BYTES on each GPU it runs on
+ * (held until the process ends), so a call allocates and frees nothing.
+ * WINO_ERR_SHAPE if wino_epilogue_workspace_bytes(batch, block_len, vocab)
+ * exceeds that size (e.g. 2 MiB holds 13107 block positions at vocab
+ * 126464).  Every call on one GPU shares that GPU's array: calls that
+ * overlap on one GPU (different streams or threads) race.  Nothing in the
+ * array needs to start at zero. */
+#define WINO_EPILOGUE_NOALLOC_MAX_BYTES (2u << 20)
+wino_status wino_epilogue_noalloc(const wino_params* p, int32_t vocab, const void* d_logits,
+                                  int32_t* d_cur_tokens, uint8_t* d_mask_bitmap, uint8_t* d_flags,
+                                  wino_row_stats* d_stats, void* stream);
+
 /* Test entry points (same kernels, unfused outputs).
  * wino_debug_logits: fp32 logits [batch, 2*block_len, vocab] of the current
  *   block rows (0..Lb-1) and shadow rows (Lb..2Lb-1) for the given state.

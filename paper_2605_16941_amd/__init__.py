@@ -14,12 +14,13 @@ import ctypes as C
 from . import _abi
 from ._abi import (WinoError, make_params, wino_create, wino_debug_forward, wino_debug_logits,
                    wino_debug_gemm, wino_decode, wino_decode_block, wino_destroy, wino_epilogue,
+                   wino_epilogue_noalloc,
                    wino_epilogue_workspace_bytes, wino_kernel_class_name, wino_last_error,
                    wino_profile, wino_profile_read, wino_row_losses, wino_status_string, wino_step,
                    wino_workspace_bytes)
 
 __all__ = ["WinoModel", "WinoError", "make_params", "wino_create", "wino_destroy", "wino_step",
-           "wino_decode_block", "wino_decode", "wino_epilogue", "wino_epilogue_workspace_bytes",
+           "wino_decode_block", "wino_decode", "wino_epilogue", "wino_epilogue_noalloc", "wino_epilogue_workspace_bytes",
            "wino_debug_logits", "wino_debug_forward", "wino_debug_gemm", "wino_profile", "wino_profile_read",
            "wino_kernel_class_name", "wino_status_string", "wino_last_error",
            "wino_row_losses", "wino_workspace_bytes"]

@@ -87,6 +87,7 @@ _protos = {
     "wino_decode": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _vp, _i32, _P(_i32), _P(_i32), _vp]),
     "wino_epilogue_workspace_bytes": (_sz, [_i32, _i32, _i32]),
     "wino_epilogue": (_i32, [_P(wino_params), _i32, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "wino_epilogue_noalloc": (_i32, [_P(wino_params), _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
     "wino_row_losses": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _vp]),
     "wino_debug_logits": (_i32, [_vp, _P(wino_params), _vp, _vp, _vp, _vp]),
     "wino_debug_forward": (_i32, [_vp, _P(wino_params), _vp, _vp, _i32, _vp, _vp]),
@@ -229,6 +230,20 @@ def wino_epilogue(p: wino_params, vocab: int, logits, cur_tokens, mask_bitmap, f
                              _ptr(flags, torch.uint8, "flags"), _ptr(stats, None, "stats"),
                              _ptr(workspace, None, "workspace"), workspace_bytes,
                              _stream(stream)), "wino_epilogue")
+
+
+EPILOGUE_NOALLOC_MAX_BYTES = 2 << 20
+
+
+def wino_epilogue_noalloc(p: wino_params, vocab: int, logits, cur_tokens, mask_bitmap, flags=None,
+                          stats=None, stream=None) -> None:
+    """wino_epilogue with the library's own per-GPU scratch (no workspace)."""
+    import torch
+    _check(lib.wino_epilogue_noalloc(C.byref(p), vocab, _ptr(logits, torch.bfloat16, "logits"),
+                                     _ptr(cur_tokens, torch.int32, "cur_tokens"),
+                                     _ptr(mask_bitmap, torch.uint8, "mask_bitmap"),
+                                     _ptr(flags, torch.uint8, "flags"), _ptr(stats, None, "stats"),
+                                     _stream(stream)), "wino_epilogue_noalloc")
 
 
 def wino_debug_logits(ctx, p: wino_params, tokens, block_start, logits, stream=None) -> None:

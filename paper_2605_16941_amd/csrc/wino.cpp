@@ -9,12 +9,21 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
 #include "kernels.h"
 
 using namespace wino;
+
+// Scratch of wino_epilogue_noalloc: the partial statistics live in this
+// file-scope device array (one copy per GPU, held until the process ends)
+// instead of a caller workspace.  In host code its name is only a host-side
+// stand-in, never a device address: host code uses the per-device address
+// from hipGetSymbolAddress (noalloc_scratch).
+constexpr size_t kNoAllocScratchBytes = WINO_EPILOGUE_NOALLOC_MAX_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
 
 namespace {
 
@@ -393,6 +402,76 @@ wino_status drain_profile(wino_ctx* c) {
   return WINO_OK;
 }
 
+// Host-side argument checks of the standalone epilogue.
+wino_status epilogue_check(const wino_params* p, int32_t vocab, const void* d_logits, const int32_t* d_cur_tokens,
+                           const uint8_t* d_mask_bitmap) {
+  if (!p || !d_logits || !d_cur_tokens || !d_mask_bitmap) return WINO_ERR_INVALID_ARG;
+  if (!std::isfinite(p->tau1) || !std::isfinite(p->tau2)) return WINO_ERR_INVALID_ARG;
+  if (p->tokens_per_step < 0) return WINO_ERR_INVALID_ARG;
+  if (p->batch < 1 || p->block_len < 1 || vocab < 8 || vocab % 8) return WINO_ERR_SHAPE;
+  if (p->mask_id < 0 || p->mask_id >= vocab) return WINO_ERR_INVALID_ARG;
+  return WINO_OK;
+}
+
+// The standalone epilogue on a given workspace: partial statistics per
+// (position, id chunk), then the merge and the decision.  Every partial the
+// decision reads is written by the statistics kernel of the same call, so the
+// workspace needs no clearing.
+wino_status epilogue_impl(const wino_params* p, int32_t vocab, const void* d_logits, int32_t* d_cur_tokens,
+                          uint8_t* d_mask_bitmap, uint8_t* d_flags, wino_row_stats* d_stats, void* d_workspace,
+                          size_t workspace_bytes, void* stream) {
+  wino_status s = epilogue_check(p, vocab, d_logits, d_cur_tokens, d_mask_bitmap);
+  if (s != WINO_OK) return s;
+  const size_t need = wino_epilogue_workspace_bytes(p->batch, p->block_len, vocab);
+  if (workspace_bytes < need) return WINO_ERR_SHAPE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int R = p->batch * p->block_len;
+  const int n_part = (vocab + kEpiChunk - 1) / kEpiChunk;
+  char* ws = static_cast<char*>(d_workspace);
+  float* pm = reinterpret_cast<float*>(ws);
+  float* ps = pm + (size_t)R * n_part;
+  float* pb = ps + (size_t)R * n_part;
+  int32_t* pi = reinterpret_cast<int32_t*>(pb + (size_t)R * n_part);
+  float* pt = reinterpret_cast<float*>(pi + (size_t)R * n_part);
+  hipError_t e = launch_epilogue_stats(static_cast<const uint16_t*>(d_logits), d_cur_tokens, p->batch,
+                                       p->block_len, vocab, p->mask_id, pm, ps, pb, pi, pt, st);
+  if (e != hipSuccess) return WINO_ERR_HIP;
+  DecideArgs da{};
+  da.pm = pm; da.ps = ps; da.pb = pb; da.pi = pi; da.pt = pt; da.n_part = n_part;
+  da.B = p->batch; da.Lb = p->block_len; da.mask_id = p->mask_id;
+  da.tau1 = p->tau1; da.tau2 = p->tau2;
+  da.force_top1 = !(p->flags & WINO_FLAG_NO_FORCE_TOP1);
+  da.cap_fill = 0; da.cap = 0;
+  da.topm = p->tokens_per_step;
+  da.standalone = 1;
+  da.tokens = d_cur_tokens;
+  da.flags = d_flags; da.bitmap = d_mask_bitmap; da.stats = d_stats;
+  e = launch_decide(da, st);
+  return e == hipSuccess ? WINO_OK : WINO_ERR_HIP;
+}
+
+// The device address of each GPU's copy of `scratch` (above), looked up once
+// per device with that device current.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+hipError_t noalloc_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
@@ -658,37 +737,23 @@ size_t wino_epilogue_workspace_bytes(int32_t batch, int32_t block_len, int32_t v
 wino_status wino_epilogue(const wino_params* p, int32_t vocab, const void* d_logits, int32_t* d_cur_tokens,
                           uint8_t* d_mask_bitmap, uint8_t* d_flags, wino_row_stats* d_stats,
                           void* d_workspace, size_t workspace_bytes, void* stream) {
-  if (!p || !d_logits || !d_cur_tokens || !d_mask_bitmap || !d_workspace) return WINO_ERR_INVALID_ARG;
-  if (!std::isfinite(p->tau1) || !std::isfinite(p->tau2)) return WINO_ERR_INVALID_ARG;
-  if (p->tokens_per_step < 0) return WINO_ERR_INVALID_ARG;
-  if (p->batch < 1 || p->block_len < 1 || vocab < 8 || vocab % 8) return WINO_ERR_SHAPE;
-  if (p->mask_id < 0 || p->mask_id >= vocab) return WINO_ERR_INVALID_ARG;
-  const size_t need = wino_epilogue_workspace_bytes(p->batch, p->block_len, vocab);
-  if (workspace_bytes < need) return WINO_ERR_SHAPE;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  const int R = p->batch * p->block_len;
-  const int n_part = (vocab + kEpiChunk - 1) / kEpiChunk;
-  char* ws = static_cast<char*>(d_workspace);
-  float* pm = reinterpret_cast<float*>(ws);
-  float* ps = pm + (size_t)R * n_part;
-  float* pb = ps + (size_t)R * n_part;
-  int32_t* pi = reinterpret_cast<int32_t*>(pb + (size_t)R * n_part);
-  float* pt = reinterpret_cast<float*>(pi + (size_t)R * n_part);
-  hipError_t e = launch_epilogue_stats(static_cast<const uint16_t*>(d_logits), d_cur_tokens, p->batch,
-                                       p->block_len, vocab, p->mask_id, pm, ps, pb, pi, pt, st);
-  if (e != hipSuccess) return WINO_ERR_HIP;
-  DecideArgs da{};
-  da.pm = pm; da.ps = ps; da.pb = pb; da.pi = pi; da.pt = pt; da.n_part = n_part;
-  da.B = p->batch; da.Lb = p->block_len; da.mask_id = p->mask_id;
-  da.tau1 = p->tau1; da.tau2 = p->tau2;
-  da.force_top1 = !(p->flags & WINO_FLAG_NO_FORCE_TOP1);
-  da.cap_fill = 0; da.cap = 0;
-  da.topm = p->tokens_per_step;
-  da.standalone = 1;
-  da.tokens = d_cur_tokens;
-  da.flags = d_flags; da.bitmap = d_mask_bitmap; da.stats = d_stats;
-  e = launch_decide(da, st);
-  return e == hipSuccess ? WINO_OK : WINO_ERR_HIP;
+  if (!d_workspace) return WINO_ERR_INVALID_ARG;
+  return epilogue_impl(p, vocab, d_logits, d_cur_tokens, d_mask_bitmap, d_flags, d_stats, d_workspace,
+                       workspace_bytes, stream);
+}
+
+wino_status wino_epilogue_noalloc(const wino_params* p, int32_t vocab, const void* d_logits,
+                                  int32_t* d_cur_tokens, uint8_t* d_mask_bitmap, uint8_t* d_flags,
+                                  wino_row_stats* d_stats, void* stream) {
+  // host-side checks first: nothing below touches the device on a rejected call
+  wino_status s = epilogue_check(p, vocab, d_logits, d_cur_tokens, d_mask_bitmap);
+  if (s != WINO_OK) return s;
+  if (wino_epilogue_workspace_bytes(p->batch, p->block_len, vocab) > kNoAllocScratchBytes)
+    return WINO_ERR_SHAPE;
+  void* ws = nullptr;
+  if (noalloc_scratch(&ws) != hipSuccess) return WINO_ERR_HIP;
+  return epilogue_impl(p, vocab, d_logits, d_cur_tokens, d_mask_bitmap, d_flags, d_stats, ws,
+                       kNoAllocScratchBytes, stream);
 }
 
 wino_status wino_debug_logits(wino_ctx* c, const wino_params* p, const int32_t* d_tokens,
