@@ -97,15 +97,17 @@ __device__ void advance_block(const DecideArgs& a, int b, int nmask_after) {
   }
 }
 
-__global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
-  extern __shared__ int smem_i[];
+// The decision of sequence b by one 256-thread workgroup (all threads call
+// it): merge the partial statistics of its block positions, then Eq. 4 (or the
+// baseline rule), the forced draft and the step cap.  smem_i holds 4*Lb ints.
+__device__ void decide_sequence(const DecideArgs& a, int b, int* smem_i) {
   int* s_cur = smem_i;                                   // [Lb] token before the step
   float* s_val = reinterpret_cast<float*>(s_cur + a.Lb);  // [Lb] conf (masked) or s (unmasked)
   int* s_hat = reinterpret_cast<int*>(s_val + a.Lb);      // [Lb] draft id
   int* s_flag = s_hat + a.Lb;                             // [Lb] decision
   __shared__ int s_nmask, s_nmask_after, s_any_draft, s_forced;
 
-  const int b = blockIdx.x, tid = threadIdx.x;
+  const int tid = threadIdx.x;
   const int Lb = a.Lb;
   RowStats* stats = reinterpret_cast<RowStats*>(a.stats);
 
@@ -264,6 +266,11 @@ __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
   advance_block(a, b, s_nmask_after);
 }
 
+__global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
+  extern __shared__ int smem_i[];
+  decide_sequence(a, blockIdx.x, smem_i);
+}
+
 // State before the first step of a call.  With advance (decode mode) a
 // sequence whose Y_cur holds no mask first moves to the first later block that
 // holds one, or to G, and its block step count restarts (a resumed or
@@ -304,31 +311,35 @@ __global__ __launch_bounds__(64) void probe_verify_kernel(const StepGeom g,
   if (lane == 0) next_verify[b] = nmask > 0 && nkeep > 0;
 }
 
-__global__ __launch_bounds__(256) void epi_stats_kernel(const uint16_t* __restrict__ logits,
-                                                        const int32_t* __restrict__ cur, int Lb, int V,
-                                                        int mask_id, float* pm, float* ps, float* pb,
-                                                        int32_t* pi, float* pt, int n_part) {
-  // Per logit the common path costs a conversion, a max, and one FMA + exp2
-  // + add for the sum; the best non-mask id is looked up afterwards only by
-  // the threads whose maximum equals the chunk's, the mask id is excluded
-  // only by the thread that holds it, and the target logit is one load.
-  constexpr int IT = kEpiChunk / (256 * 8);
+// Partial softmax statistics of one chunk of CHUNK ids of one needed logits
+// row r (the current row of a masked position, the shadow row of an unmasked
+// one), written by thread 0 to slot (r, chunk) of the partial arrays.
+// Per logit the common path costs a conversion, a max, and one FMA + exp2 +
+// add for the sum; the best non-mask id is looked up afterwards only by the
+// threads whose maximum equals the chunk's, the mask id is excluded only by
+// the thread that holds it, and the target logit is one load.
+template <int CHUNK>
+__device__ void chunk_stats(const uint16_t* __restrict__ logits, const int32_t* __restrict__ cur, int Lb,
+                            int V, int mask_id, int r, int chunk, int n_part, float* pm, float* ps,
+                            float* pb, int32_t* pi, float* pt) {
+  constexpr int IT = CHUNK / (256 * 8);
+  constexpr int STRIDE = 256 * 8;  // ids between a thread's consecutive 16-byte loads
   constexpr float kLog2e = 1.4426950408889634f;
   __shared__ float red[3][4];
   __shared__ int redi[4];
-  const int r = blockIdx.y, chunk = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = r / Lb, l = r - b * Lb;
   const int tok = cur[r];
   const bool masked = tok == mask_id;
   const uint16_t* row = logits + ((size_t)b * 2 * Lb + (masked ? l : Lb + l)) * V;
   const int tgt = masked ? -1 : tok;
-  const int v0 = chunk * kEpiChunk;
-  const int v1 = min(V, v0 + kEpiChunk);
+  const int v0 = chunk * CHUNK;
+  const int v1 = min(V, v0 + CHUNK);
 
   uint4 raw[IT];
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
-    const int idx = v0 + (it * 256 + tid) * 8;
+    const int idx = v0 + it * STRIDE + tid * 8;
     raw[it] = idx < v1 ? *reinterpret_cast<const uint4*>(row + idx) : make_uint4(0xFF7FFF7Fu, 0xFF7FFF7Fu, 0xFF7FFF7Fu, 0xFF7FFF7Fu);
   }
   // (ids past V read as the most negative finite bf16 and never win)
@@ -343,14 +354,14 @@ __global__ __launch_bounds__(256) void epi_stats_kernel(const uint16_t* __restri
     for (int e = 0; e < 8; ++e) mx = fmaxf(mx, elem(it, e));
   // best value over non-mask ids: differs from mx only in the thread holding mask_id
   float nm = mx;
-  const int my0 = v0 + tid * 8;  // this thread's ids: my0 + it*2048 + e
-  if (mask_id >= v0 && mask_id < v1 && (mask_id - my0) >= 0 && ((mask_id - my0) & 2047) < 8) {
+  const int my0 = v0 + tid * 8;  // this thread's ids: my0 + it*STRIDE + e
+  if (mask_id >= v0 && mask_id < v1 && (mask_id - my0) >= 0 && ((mask_id - my0) % STRIDE) < 8) {
     nm = kNegBig;
 #pragma unroll
     for (int it = 0; it < IT; ++it)
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        if (my0 + it * 2048 + e != mask_id) nm = fmaxf(nm, elem(it, e));
+        if (my0 + it * STRIDE + e != mask_id) nm = fmaxf(nm, elem(it, e));
   }
   float m = wave_max(mx), bz = wave_max(nm);
   if (lane == 0) { red[0][wave] = m; red[1][wave] = bz; }
@@ -364,7 +375,7 @@ __global__ __launch_bounds__(256) void epi_stats_kernel(const uint16_t* __restri
     for (int it = IT - 1; it >= 0; --it)
 #pragma unroll
       for (int e = 7; e >= 0; --e) {
-        const int id = my0 + it * 2048 + e;
+        const int id = my0 + it * STRIDE + e;
         if (id < v1 && id != mask_id && elem(it, e) == bz) bi = id;
       }
   }
@@ -388,6 +399,19 @@ __global__ __launch_bounds__(256) void epi_stats_kernel(const uint16_t* __restri
     const size_t o = (size_t)r * n_part + chunk;
     pm[o] = m; ps[o] = s; pb[o] = bz; pi[o] = ii; pt[o] = tt;
   }
+}
+
+// Standalone epilogue statistics: workgroup (chunk, r) writes the partial
+// statistics of its chunk of row r; decide_kernel then merges and decides.
+// (One launch, with the last workgroup of each sequence deciding, was 2.7-6x
+// slower: the device-scope release each workgroup needs before counting
+// itself done writes back its XCD's L2.)
+template <int CHUNK>
+__global__ __launch_bounds__(256) void epi_stats_kernel(const uint16_t* __restrict__ logits,
+                                                        const int32_t* __restrict__ cur, int Lb, int V,
+                                                        int mask_id, float* pm, float* ps, float* pb,
+                                                        int32_t* pi, float* pt, int n_part) {
+  chunk_stats<CHUNK>(logits, cur, Lb, V, mask_id, blockIdx.y, blockIdx.x, n_part, pm, ps, pb, pi, pt);
 }
 
 }  // namespace
@@ -459,7 +483,8 @@ hipError_t launch_epilogue_stats(const uint16_t* logits, const int32_t* cur_toke
                                  float* pt, hipStream_t st) {
   const int n_part = (V + kEpiChunk - 1) / kEpiChunk;
   dim3 grid(n_part, B * Lb);
-  epi_stats_kernel<<<grid, 256, 0, st>>>(logits, cur_tokens, Lb, V, mask_id, pm, ps, pb, pi, pt, n_part);
+  epi_stats_kernel<kEpiChunk><<<grid, 256, 0, st>>>(logits, cur_tokens, Lb, V, mask_id, pm, ps, pb, pi, pt,
+                                                    n_part);
   return hipGetLastError();
 }
 

@@ -293,12 +293,17 @@ def test_epilogue_contract(P, B, lb, V, heights):
     logits, cur, _ = wi.epilogue_inputs(B, lb, V, mask, seed=2, heights=heights, device="cuda")
     cur0 = cur.cpu().numpy()
     prm = P.make_params(B, 1, lb, lb, mask, 0.7, 0.9)
-    ws = torch.empty(P.wino_epilogue_workspace_bytes(B, lb, V), dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(P.wino_epilogue_workspace_bytes(B, lb, V), dtype=torch.uint8, device="cuda")
     bitmap = torch.full((B, lb), 9, dtype=torch.uint8, device="cuda")
     flags = torch.full((B, lb), 9, dtype=torch.uint8, device="cuda")
     stats = torch.zeros(B * lb * STATS_DT.itemsize, dtype=torch.uint8, device="cuda")
+    cur_again = cur.clone()
     P.wino_epilogue(prm, V, logits, cur, bitmap, flags, stats, ws)
+    # a second call on the same workspace gives the same result
+    bitmap2 = torch.full((B, lb), 9, dtype=torch.uint8, device="cuda")
+    P.wino_epilogue(prm, V, logits, cur_again, bitmap2, workspace=ws)
     torch.cuda.synchronize()
+    assert torch.equal(cur_again, cur) and torch.equal(bitmap2, bitmap)
     ref = E.decide(logits.cpu(), cur0, mask, float(np.float32(0.7)), float(np.float32(0.9)))
     gt, gb, gf = cur.cpu().numpy(), bitmap.cpu().numpy(), flags.cpu().numpy()
     st = stats.cpu().numpy().view(STATS_DT).reshape(B, lb)

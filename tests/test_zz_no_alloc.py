@@ -33,7 +33,7 @@ def run_both(P, B, lb, V, heights, seed):
         if noalloc:
             P.wino_epilogue_noalloc(prm, V, logits, c, bitmap, flags, stats)
         else:
-            ws = torch.empty(P.wino_epilogue_workspace_bytes(B, lb, V), dtype=torch.uint8, device="cuda")
+            ws = torch.zeros(P.wino_epilogue_workspace_bytes(B, lb, V), dtype=torch.uint8, device="cuda")
             P.wino_epilogue(prm, V, logits, c, bitmap, flags, stats, ws)
         torch.cuda.synchronize()
         outs.append((c.cpu(), bitmap.cpu(), flags.cpu(), stats.cpu()))
