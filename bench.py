@@ -238,10 +238,18 @@ def run_epilogue(P, wi, n_calls=20, n_buf=4):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / n_calls
     algo = B * lb * V * 2  # one bf16 row per position is read (Eq. 4)
-    return {"workload": f"standalone epilogue, logits [{B}, {2 * lb}, {V}] bf16, {n_buf} rotating buffers",
-            "ms_per_call": round(ms, 4), "algorithmic_bytes": algo,
-            "gbs": round(algo / (ms * 1e-3) / 1e9, 1),
-            "hbm_frac": round(algo / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+    out = {"workload": f"standalone epilogue, logits [{B}, {2 * lb}, {V}] bf16, {n_buf} rotating buffers",
+           "ms_per_call": round(ms, 4), "algorithmic_bytes": algo,
+           "gbs": round(algo / (ms * 1e-3) / 1e9, 1),
+           "hbm_frac": round(algo / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4), "traffic": None}
+    rec = _summary(MEMBOUND_FILE, MEMBOUND_SOURCES)
+    try:
+        t = float(rec["epilogue.epilogue_stats.bytes_per_launch"]) + float(rec["epilogue.decide.bytes_per_launch"])
+        out.update({"traffic": round(t), "traffic_gbs": round(t / (ms * 1e-3) / 1e9, 1),
+                    "traffic_hbm_frac": round(t / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)})
+    except (TypeError, KeyError, ValueError):
+        pass
+    return out
 
 
 def mmada_cpu_sample(wi, cfg, weights, name):
