@@ -58,9 +58,14 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
   static_assert(NS >= 2, "pipeline stages");
   __shared__ __attribute__((aligned(1024))) uint16_t smem[NS * STAGE];
 
-  const int b = blockIdx.z, h = blockIdx.y;
+  // Workgroups are dealt to the 8 XCDs round-robin; remapped, each XCD takes a
+  // contiguous range of (query tile, head, sequence) ids, so the query tiles
+  // of one head share that XCD's L2 copy of its K and V^T
+  const int nqt = gridDim.x, nwg = nqt * gridDim.y * gridDim.z;
+  const int lin = xcd_remap(blockIdx.x + nqt * (blockIdx.y + gridDim.y * blockIdx.z), nwg);
+  const int qt = lin % nqt, h = (lin / nqt) % gridDim.y, b = lin / (nqt * gridDim.y);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, grp = lane >> 5;
-  const int q0 = blockIdx.x * (NW * 32);
+  const int q0 = qt * (NW * 32);
   const int c0 = cur_start(g, b);
   const int NQ = g.Lb + g.Ls;                    // compact queries per sequence
   const int ci = q0 + wave * 32 + (lane & 31);   // compact query index (CQ)
@@ -170,6 +175,12 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
     // S^T for the two 32-key blocks: the two MFMA chains alternate, and the
     // K fragments of step ks + 2 are read while step ks multiplies (one step
     // ahead leaves the LDS latency exposed: bs16 133 -> 131 us, two steps 129)
+    auto vfrag = [&](int ks4, int fe) {
+      const int row = fe * 32 + (lane & 31);
+      const int ch = (ks4 * 2 + grp) ^ vswz[fe];
+      return as_bf16x8(*reinterpret_cast<const uint4*>(sV + row * BKV + ch * 8));
+    };
+    bf16x8 vf[2][FE];
     f32x16 s[2];
 #pragma unroll
     for (int kb2 = 0; kb2 < 2; ++kb2)
@@ -184,15 +195,23 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
     kf[0][1] = kfrag(0, 1);
     kf[1][0] = kfrag(1, 0);
     kf[1][1] = kfrag(1, 1);
+    // the order is pinned: left to itself the compiler keeps one fragment
+    // set and waits for each pair of reads right before its MFMAs
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 1);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       if (ks + 2 < KS) {
         kf[(ks + 2) % 3][0] = kfrag(ks + 2, 0);
         kf[(ks + 2) % 3][1] = kfrag(ks + 2, 1);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
       }
       s[0] = mfma32(kf[ks % 3][0], qf[ks], s[0]);
       s[1] = mfma32(kf[ks % 3][1], qf[ks], s[1]);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 1);
     }
+    // the first V^T fragments load while the softmax runs
+#pragma unroll
+    for (int fe = 0; fe < FE; ++fe) vf[0][fe] = vfrag(0, fe);
 
     // Only tiles that reach past S or hold an excluded shadow column need the
     // mask predicate; the test is uniform over the workgroup.
@@ -246,6 +265,11 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
 
 #pragma unroll
     for (int ks4 = 0; ks4 < BKV / 16; ++ks4) {
+      // V^T fragments of the next 16-key step are read while this one multiplies
+      if (ks4 + 1 < BKV / 16) {
+#pragma unroll
+        for (int fe = 0; fe < FE; ++fe) vf[(ks4 + 1) & 1][fe] = vfrag(ks4 + 1, fe);
+      }
       // P in bf16: registers 8*(ks4&1)..+7 of block ks4/2 hold keys
       // 16*ks4 + 8*grp + 0..7.
       const int base = 8 * (ks4 & 1);
@@ -255,12 +279,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
         ph[e] = pack2bf(s[ks4 >> 1][base + 2 * e], s[ks4 >> 1][base + 2 * e + 1]);
       const bf16x8 pf = as_bf16x8(make_uint4(ph[0], ph[1], ph[2], ph[3]));
 #pragma unroll
-      for (int fe = 0; fe < FE; ++fe) {
-        const int row = fe * 32 + (lane & 31);
-        const int ch = (ks4 * 2 + grp) ^ vswz[fe];
-        const bf16x8 vf = as_bf16x8(*reinterpret_cast<const uint4*>(sV + row * BKV + ch * 8));
-        oacc[fe] = mfma32(vf, pf, oacc[fe]);
-      }
+      for (int fe = 0; fe < FE; ++fe) oacc[fe] = mfma32(vf[ks4 & 1][fe], pf, oacc[fe]);
     }
   }
 
