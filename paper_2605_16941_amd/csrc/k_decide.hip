@@ -97,9 +97,32 @@ __device__ void advance_block(const DecideArgs& a, int b, int nmask_after) {
   }
 }
 
+// Lanes per block position in the partial merge: the largest power of two
+// (at most 64) with lanes * Lb <= 256, so one pass covers the block when
+// Lb <= 256.
+__host__ __device__ __forceinline__ int merge_lanes(int Lb) {
+  int gs = 1;
+  while (gs < 64 && gs * 2 * Lb <= 256) gs *= 2;
+  return gs;
+}
+
+// Partials j0, j0 + gs, ..., j0 + (U-1)*gs of row `row` (indices past n_part
+// read partial 0 again and are not merged).
+template <int U>
+__device__ __forceinline__ void load_parts(const DecideArgs& a, size_t row, int j0, int gs, Part (&q)[U]) {
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int j = j0 + u * gs;
+    const size_t o = row * a.n_part + (j < a.n_part ? j : 0);
+    q[u] = Part{a.pm[o], a.ps[o], a.pb[o], a.pt[o], a.pi[o]};
+  }
+}
+
 // The decision of sequence b by one 256-thread workgroup (all threads call
 // it): merge the partial statistics of its block positions, then Eq. 4 (or the
 // baseline rule), the forced draft and the step cap.  smem_i holds 4*Lb ints.
+// U: partials each merge lane loads at once.
+template <int U>
 __device__ void decide_sequence(const DecideArgs& a, int b, int* smem_i) {
   int* s_cur = smem_i;                                   // [Lb] token before the step
   float* s_val = reinterpret_cast<float*>(s_cur + a.Lb);  // [Lb] conf (masked) or s (unmasked)
@@ -124,6 +147,12 @@ __device__ void decide_sequence(const DecideArgs& a, int b, int* smem_i) {
     cur_ptr = a.tokens + (size_t)b * a.S + a.P + bsc;
     if (a.final_step && a.seq_steps) fin_ptr = a.final_step + (size_t)b * a.G + bsc;
   }
+  // The first batch of partial loads goes out before the token loads, so the
+  // two memory round trips overlap.
+  const int gs = merge_lanes(Lb), per_pass = 256 / gs;
+  const int sl = tid & (gs - 1);
+  Part q0[U];
+  load_parts<U>(a, (size_t)b * Lb + (tid / gs < Lb ? tid / gs : 0), sl, gs, q0);
   if (tid == 0) { s_nmask = 0; s_nmask_after = 0; s_any_draft = 0; s_forced = -1; }
   __syncthreads();
   if (!done) {
@@ -156,25 +185,19 @@ __device__ void decide_sequence(const DecideArgs& a, int b, int* smem_i) {
   }
 
   // merge partials: a group of gs lanes per position, every position of a
-  // pass at once (gs * positions = 256), so the partial loads of all
-  // positions are in flight together
-  int gs = 1;
-  while (gs < 64 && gs * 2 * Lb <= 256) gs *= 2;
-  const int per_pass = 256 / gs;
+  // pass at once, U partials' loads in flight per lane before they merge
   for (int base = 0; base < Lb; base += per_pass) {
-    const int l = base + tid / gs, sl = tid & (gs - 1);
+    const int l = base + tid / gs;
     const size_t row = (size_t)b * Lb + (l < Lb ? l : 0);
     Part p = {kNegBig, 0.f, kNegBig, kNegBig, INT_MAX};
     if (l < Lb) {
-      // eight partials' loads in flight per lane before they are merged
-      constexpr int U = 8;
       for (int j0 = sl; j0 < a.n_part; j0 += gs * U) {
         Part q[U];
+        if (base == 0 && j0 == sl) {
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int j = j0 + u * gs;
-          const size_t o = row * a.n_part + (j < a.n_part ? j : 0);
-          q[u] = Part{a.pm[o], a.ps[o], a.pb[o], a.pt[o], a.pi[o]};
+          for (int u = 0; u < U; ++u) q[u] = q0[u];
+        } else {
+          load_parts<U>(a, row, j0, gs, q);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u)
@@ -266,9 +289,10 @@ __device__ void decide_sequence(const DecideArgs& a, int b, int* smem_i) {
   advance_block(a, b, s_nmask_after);
 }
 
+template <int U>
 __global__ __launch_bounds__(256) void decide_kernel(const DecideArgs a) {
   extern __shared__ int smem_i[];
-  decide_sequence(a, blockIdx.x, smem_i);
+  decide_sequence<U>(a, blockIdx.x, smem_i);
 }
 
 // State before the first step of a call.  With advance (decode mode) a
@@ -318,6 +342,39 @@ __global__ __launch_bounds__(64) void probe_verify_kernel(const StepGeom g,
 // add for the sum; the best non-mask id is looked up afterwards only by the
 // threads whose maximum equals the chunk's, the mask id is excluded only by
 // the thread that holds it, and the target logit is one load.
+// Wave-wide reductions on VALU alone (no LDS round trip per step): xor 1 and
+// xor 2 inside quads and the half-row and row mirrors by DPP, then rows
+// 0<->1, 2<->3 (permlane16_swap) and the two 32-lane halves (permlane32_swap).
+// Every lane ends with the result.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+template <class Op>
+__device__ __forceinline__ uint32_t valu_wave_reduce(uint32_t v, Op op) {
+  v = op(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = op(v, dpp<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = op(v, dpp<0x141>(v));  // row_half_mirror
+  v = op(v, dpp<0x140>(v));  // row_mirror
+  auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  v = op(r[0], r[1]);
+  r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return op(r[0], r[1]);
+}
+__device__ __forceinline__ float valu_wave_max(float x) {
+  return __uint_as_float(valu_wave_reduce(__float_as_uint(x), [](uint32_t a, uint32_t b) {
+    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
+  }));
+}
+__device__ __forceinline__ float valu_wave_sum(float x) {
+  return __uint_as_float(valu_wave_reduce(__float_as_uint(x), [](uint32_t a, uint32_t b) {
+    return __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
+  }));
+}
+__device__ __forceinline__ int valu_wave_min(int x) {
+  return (int)valu_wave_reduce((uint32_t)x, [](uint32_t a, uint32_t b) { return (uint32_t)min((int)a, (int)b); });
+}
+
 template <int CHUNK>
 __device__ void chunk_stats(const uint16_t* __restrict__ logits, const int32_t* __restrict__ cur, int Lb,
                             int V, int mask_id, int r, int chunk, int n_part, float* pm, float* ps,
@@ -335,6 +392,10 @@ __device__ void chunk_stats(const uint16_t* __restrict__ logits, const int32_t* 
   const int tgt = masked ? -1 : tok;
   const int v0 = chunk * CHUNK;
   const int v1 = min(V, v0 + CHUNK);
+  // the target logit's load goes out with the chunk's, every lane reading the
+  // same address (a chunk without the target reads its first id, unused)
+  const bool has_tgt = tgt >= v0 && tgt < v1;
+  const uint16_t t_raw = row[has_tgt ? tgt : v0];
 
   uint4 raw[IT];
 #pragma unroll
@@ -363,7 +424,9 @@ __device__ void chunk_stats(const uint16_t* __restrict__ logits, const int32_t* 
       for (int e = 0; e < 8; ++e)
         if (my0 + it * STRIDE + e != mask_id) nm = fmaxf(nm, elem(it, e));
   }
-  float m = wave_max(mx), bz = wave_max(nm);
+  // bz differs from m only in the chunk holding mask_id
+  const bool mask_here = mask_id >= v0 && mask_id < v1;
+  float m = valu_wave_max(mx), bz = mask_here ? valu_wave_max(nm) : m;
   if (lane == 0) { red[0][wave] = m; red[1][wave] = bz; }
   __syncthreads();
   m = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
@@ -387,15 +450,14 @@ __device__ void chunk_stats(const uint16_t* __restrict__ logits, const int32_t* 
   for (int it = 0; it < IT; ++it)
 #pragma unroll
     for (int e = 0; e < 8; ++e) se += __builtin_amdgcn_exp2f(fmaf(elem(it, e), kLog2e, -mc));
-  se = wave_sum(se);
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) bi = min(bi, __shfl_xor(bi, o, 64));
+  se = valu_wave_sum(se);
+  bi = valu_wave_min(bi);
   if (lane == 0) { red[2][wave] = se; redi[wave] = bi; }
   __syncthreads();
   if (tid == 0) {
     const float s = (red[2][0] + red[2][1]) + (red[2][2] + red[2][3]);
     const int ii = min(min(redi[0], redi[1]), min(redi[2], redi[3]));
-    const float tt = tgt >= v0 && tgt < v1 ? bf2f(row[tgt]) : kNegBig;
+    const float tt = has_tgt ? bf2f(t_raw) : kNegBig;
     const size_t o = (size_t)r * n_part + chunk;
     pm[o] = m; ps[o] = s; pb[o] = bz; pi[o] = ii; pt[o] = tt;
   }
@@ -474,7 +536,10 @@ hipError_t launch_probe_verify(const StepGeom& g, const int32_t* tokens, int32_t
 
 hipError_t launch_decide(const DecideArgs& a, hipStream_t st) {
   const size_t shm = (size_t)a.Lb * 16;
-  decide_kernel<<<a.B, 256, shm, st>>>(a);
+  // U = 2 covers up to 2*gs partials per position in one batch (the
+  // standalone epilogue); the LM head's many vocabulary tiles take batches of 8
+  if (a.n_part <= 2 * merge_lanes(a.Lb)) decide_kernel<2><<<a.B, 256, shm, st>>>(a);
+  else decide_kernel<8><<<a.B, 256, shm, st>>>(a);
   return hipGetLastError();
 }
 

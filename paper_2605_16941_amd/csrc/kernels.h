@@ -191,7 +191,7 @@ hipError_t launch_probe_verify(const StepGeom& g, const int32_t* tokens, int32_t
 // Standalone epilogue statistics: for each (b, l) pick the current row
 // (masked) or the shadow row (unmasked) of bf16 logits [B, 2Lb, V], and write
 // partials over chunks of kEpiChunk ids.
-constexpr int kEpiChunk = 16384;
+constexpr int kEpiChunk = 8192;
 hipError_t launch_epilogue_stats(const uint16_t* logits, const int32_t* cur_tokens, int B, int Lb,
                                  int V, int mask_id, float* pm, float* ps, float* pb, int32_t* pi,
                                  float* pt, hipStream_t st);
