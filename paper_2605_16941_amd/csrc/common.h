@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace wino {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
@@ -46,6 +48,77 @@ __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
   return v;
+}
+
+// Reductions on the vector ALU alone, without the LDS round trip of a
+// shuffle per step: DPP lane swaps inside quads (xor 1, xor 2), the half-row
+// and row mirrors (groups of 8 and 16 lanes), then rows 0<->1 and 2<->3
+// (v_permlane16_swap: groups of 32) and the two halves (v_permlane32_swap:
+// 64).  op must be commutative and associative; every lane of a group ends
+// with the group's result (both lanes of each pair combine the same two
+// values).
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+template <int LANES, class Op>
+__device__ __forceinline__ uint32_t valu_reduce(uint32_t v, Op op) {
+  static_assert(LANES == 32 || LANES == 64, "groups of 32 or 64 lanes");
+  v = op(v, dpp_mov<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = op(v, dpp_mov<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = op(v, dpp_mov<0x141>(v));  // row_half_mirror
+  v = op(v, dpp_mov<0x140>(v));  // row_mirror
+  auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  v = op(r[0], r[1]);
+  if constexpr (LANES == 64) {
+    r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    v = op(r[0], r[1]);
+  }
+  return v;
+}
+template <int LANES>
+__device__ __forceinline__ float valu_max(float x) {
+  return __uint_as_float(valu_reduce<LANES>(__float_as_uint(x), [](uint32_t a, uint32_t b) {
+    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
+  }));
+}
+template <int LANES>
+__device__ __forceinline__ float valu_sum(float x) {
+  return __uint_as_float(valu_reduce<LANES>(__float_as_uint(x), [](uint32_t a, uint32_t b) {
+    return __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
+  }));
+}
+template <int LANES>
+__device__ __forceinline__ int valu_min(int x) {
+  return (int)valu_reduce<LANES>((uint32_t)x, [](uint32_t a, uint32_t b) { return (uint32_t)min((int)a, (int)b); });
+}
+// (value, id) pairs: the largest value, the lowest id among equal values.
+template <int LANES>
+__device__ __forceinline__ void valu_argmax(float& v, int& id) {
+  auto take = [&](float ov, int oi) {
+    if (ov > v || (ov == v && oi < id)) { v = ov; id = oi; }
+  };
+  auto step = [&](auto ctrl) {
+    constexpr int C = decltype(ctrl)::value;
+    take(__uint_as_float(dpp_mov<C>(__float_as_uint(v))), (int)dpp_mov<C>((uint32_t)id));
+  };
+  step(std::integral_constant<int, 0xB1>{});
+  step(std::integral_constant<int, 0x4E>{});
+  step(std::integral_constant<int, 0x141>{});
+  step(std::integral_constant<int, 0x140>{});
+  auto swap = [&](auto rv, auto ri) {
+    // rv / ri: this lane's value and its partner's, in some order
+    const float a = __uint_as_float(rv[0]), b = __uint_as_float(rv[1]);
+    const int ia = (int)ri[0], ib = (int)ri[1];
+    const bool second = b > a || (b == a && ib < ia);
+    v = second ? b : a;
+    id = second ? ib : ia;
+  };
+  swap(__builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false),
+       __builtin_amdgcn_permlane16_swap((uint32_t)id, (uint32_t)id, false, false));
+  if constexpr (LANES == 64)
+    swap(__builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false),
+         __builtin_amdgcn_permlane32_swap((uint32_t)id, (uint32_t)id, false, false));
 }
 
 // Reductions over the lane pair (l, l ^ 32): v_permlane32_swap exchanges the

@@ -342,39 +342,6 @@ __global__ __launch_bounds__(64) void probe_verify_kernel(const StepGeom g,
 // add for the sum; the best non-mask id is looked up afterwards only by the
 // threads whose maximum equals the chunk's, the mask id is excluded only by
 // the thread that holds it, and the target logit is one load.
-// Wave-wide reductions on VALU alone (no LDS round trip per step): xor 1 and
-// xor 2 inside quads and the half-row and row mirrors by DPP, then rows
-// 0<->1, 2<->3 (permlane16_swap) and the two 32-lane halves (permlane32_swap).
-// Every lane ends with the result.
-template <int CTRL>
-__device__ __forceinline__ uint32_t dpp(uint32_t v) {
-  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
-}
-template <class Op>
-__device__ __forceinline__ uint32_t valu_wave_reduce(uint32_t v, Op op) {
-  v = op(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]
-  v = op(v, dpp<0x4E>(v));   // quad_perm [2,3,0,1]
-  v = op(v, dpp<0x141>(v));  // row_half_mirror
-  v = op(v, dpp<0x140>(v));  // row_mirror
-  auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
-  v = op(r[0], r[1]);
-  r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-  return op(r[0], r[1]);
-}
-__device__ __forceinline__ float valu_wave_max(float x) {
-  return __uint_as_float(valu_wave_reduce(__float_as_uint(x), [](uint32_t a, uint32_t b) {
-    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
-  }));
-}
-__device__ __forceinline__ float valu_wave_sum(float x) {
-  return __uint_as_float(valu_wave_reduce(__float_as_uint(x), [](uint32_t a, uint32_t b) {
-    return __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
-  }));
-}
-__device__ __forceinline__ int valu_wave_min(int x) {
-  return (int)valu_wave_reduce((uint32_t)x, [](uint32_t a, uint32_t b) { return (uint32_t)min((int)a, (int)b); });
-}
-
 template <int CHUNK>
 __device__ void chunk_stats(const uint16_t* __restrict__ logits, const int32_t* __restrict__ cur, int Lb,
                             int V, int mask_id, int r, int chunk, int n_part, float* pm, float* ps,
@@ -426,7 +393,7 @@ __device__ void chunk_stats(const uint16_t* __restrict__ logits, const int32_t* 
   }
   // bz differs from m only in the chunk holding mask_id
   const bool mask_here = mask_id >= v0 && mask_id < v1;
-  float m = valu_wave_max(mx), bz = mask_here ? valu_wave_max(nm) : m;
+  float m = valu_max<64>(mx), bz = mask_here ? valu_max<64>(nm) : m;
   if (lane == 0) { red[0][wave] = m; red[1][wave] = bz; }
   __syncthreads();
   m = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
@@ -450,8 +417,8 @@ __device__ void chunk_stats(const uint16_t* __restrict__ logits, const int32_t* 
   for (int it = 0; it < IT; ++it)
 #pragma unroll
     for (int e = 0; e < 8; ++e) se += __builtin_amdgcn_exp2f(fmaf(elem(it, e), kLog2e, -mc));
-  se = valu_wave_sum(se);
-  bi = valu_wave_min(bi);
+  se = valu_sum<64>(se);
+  bi = valu_min<64>(bi);
   if (lane == 0) { red[2][wave] = se; redi[wave] = bi; }
   __syncthreads();
   if (tid == 0) {

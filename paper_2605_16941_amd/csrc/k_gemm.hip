@@ -337,7 +337,8 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
           // lane pairs trade one value: the even lane stores elements e, e+1,
           // the odd lane elements e+hd/2-1, e+hd/2 (one 4-byte write each)
           const bool odd = lane & 1;
-          const float got = __shfl_xor(odd ? r1 : r2, 1, 64);
+          // (lane ^ 1 by a DPP quad swap, no LDS round trip)
+          const float got = __uint_as_float(dpp_mov<0xB1>(__float_as_uint(odd ? r1 : r2)));
           const int ee = odd ? e + half - 1 : e;
           const uint32_t pk = odd ? pack2bf(got, r2) : pack2bf(r1, got);
           *reinterpret_cast<uint32_t*>(wr + (((ee >> 3) ^ sw) << 3) + (ee & 7)) = pk;
@@ -478,14 +479,10 @@ __device__ __forceinline__ void epi_lmstats(const GemmCall& c, f32x16 (&acc)[FM]
         if (col != lm.mask_id && v > bz) { bz = v; bi = col; }
         if (col == tgt) tz = v;
       }
-#pragma unroll
-      for (int o = 16; o > 0; o >>= 1) {
-        mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-        tz = fmaxf(tz, __shfl_xor(tz, o, 64));
-        const float ob = __shfl_xor(bz, o, 64);
-        const int oi = __shfl_xor(bi, o, 64);
-        if (ob > bz || (ob == bz && oi < bi)) { bz = ob; bi = oi; }
-      }
+      // over the 32 lanes (columns) of each half-wave
+      mx = valu_max<32>(mx);
+      tz = valu_max<32>(tz);
+      valu_argmax<32>(bz, bi);
       float se = 0.f, sz = 0.f;
       if (lm.pz) {
         // sum exp(z - m) * (z - m): the entropy's expectation term, relative
@@ -497,16 +494,12 @@ __device__ __forceinline__ void epi_lmstats(const GemmCall& c, f32x16 (&acc)[FM]
           se += e;
           sz += e * u;
         }
-#pragma unroll
-        for (int o = 16; o > 0; o >>= 1) {
-          se += __shfl_xor(se, o, 64);
-          sz += __shfl_xor(sz, o, 64);
-        }
+        se = valu_sum<32>(se);
+        sz = valu_sum<32>(sz);
       } else {
 #pragma unroll
         for (int fn = 0; fn < FN; ++fn) se += __expf(acc[fm][fn][i] + bias[fn] - mx);
-#pragma unroll
-        for (int o = 16; o > 0; o >>= 1) se += __shfl_xor(se, o, 64);
+        se = valu_sum<32>(se);
       }
       if ((lane & 31) == 0) {
         red_m[wn * BM + lrow] = mx;
