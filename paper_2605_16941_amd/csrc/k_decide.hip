@@ -147,12 +147,14 @@ __device__ void decide_sequence(const DecideArgs& a, int b, int* smem_i) {
     cur_ptr = a.tokens + (size_t)b * a.S + a.P + bsc;
     if (a.final_step && a.seq_steps) fin_ptr = a.final_step + (size_t)b * a.G + bsc;
   }
-  // The first batch of partial loads goes out before the token loads, so the
-  // two memory round trips overlap.
+  // With one batch per lane (PRE: the launch guarantees n_part <= gs * U and
+  // Lb <= 256) the partial loads go out before the token loads, so the two
+  // memory round trips overlap; otherwise the batches load in the merge loop.
+  constexpr bool PRE = U == 2;
   const int gs = merge_lanes(Lb), per_pass = 256 / gs;
   const int sl = tid & (gs - 1);
   Part q0[U];
-  load_parts<U>(a, (size_t)b * Lb + (tid / gs < Lb ? tid / gs : 0), sl, gs, q0);
+  if constexpr (PRE) load_parts<U>(a, (size_t)b * Lb + (tid / gs < Lb ? tid / gs : 0), sl, gs, q0);
   if (tid == 0) { s_nmask = 0; s_nmask_after = 0; s_any_draft = 0; s_forced = -1; }
   __syncthreads();
   if (!done) {
@@ -193,7 +195,7 @@ __device__ void decide_sequence(const DecideArgs& a, int b, int* smem_i) {
     if (l < Lb) {
       for (int j0 = sl; j0 < a.n_part; j0 += gs * U) {
         Part q[U];
-        if (base == 0 && j0 == sl) {
+        if constexpr (PRE) {
 #pragma unroll
           for (int u = 0; u < U; ++u) q[u] = q0[u];
         } else {
@@ -505,7 +507,7 @@ hipError_t launch_decide(const DecideArgs& a, hipStream_t st) {
   const size_t shm = (size_t)a.Lb * 16;
   // U = 2 covers up to 2*gs partials per position in one batch (the
   // standalone epilogue); the LM head's many vocabulary tiles take batches of 8
-  if (a.n_part <= 2 * merge_lanes(a.Lb)) decide_kernel<2><<<a.B, 256, shm, st>>>(a);
+  if (a.n_part <= 2 * merge_lanes(a.Lb) && a.Lb <= 256) decide_kernel<2><<<a.B, 256, shm, st>>>(a);
   else decide_kernel<8><<<a.B, 256, shm, st>>>(a);
   return hipGetLastError();
 }
