@@ -227,7 +227,7 @@ wino_status wino_epilogue(const wino_params* p, int32_t vocab, const void* d_log
  * device array of WINO_EPILOGUE_NOALLOC_MAX_BYTES on each GPU it runs on
  * (held until the process ends), so a call allocates and frees nothing.
  * WINO_ERR_SHAPE if wino_epilogue_workspace_bytes(batch, block_len, vocab)
- * exceeds that size (e.g. 2 MiB holds 13107 block positions at vocab
+ * exceeds that size (e.g. 2 MiB holds 6552 block positions at vocab
  * 126464).  Every call on one GPU shares that GPU's array: calls that
  * overlap on one GPU (different streams or threads) race.  Nothing in the
  * array needs to start at zero. */

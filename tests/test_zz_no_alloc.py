@@ -54,7 +54,7 @@ def test_noalloc_epilogue_matches_workspace_entry_point(P):
 
 
 def test_noalloc_epilogue_rejects_inputs_beyond_its_scratch(P):
-    # 128 x 128 positions at vocab 126464 need 2.6 MB of partials > 2 MiB:
+    # 128 x 128 positions at vocab 126464 need 5.2 MB of partials > 2 MiB:
     # rejected on the host before any device work
     B, lb, V = 128, 128, 126464
     assert P.wino_epilogue_workspace_bytes(B, lb, V) > P._abi.EPILOGUE_NOALLOC_MAX_BYTES
