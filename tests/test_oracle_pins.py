@@ -466,6 +466,65 @@ def test_full_diffusion_is_a_single_block(tiny_weights):
     assert not np.any(out == cfg.mask_id)
 
 
+def test_margins_and_top2_gap_closed_forms():
+    """The quantities that choose which positions a parity test compares
+    (Eq. 2-4): on logits whose softmax is known in closed form, the draft
+    confidence, the verify probability, the margin of each from its threshold
+    and the top-2 gap over ids other than the mask equal their closed forms.
+    The mask id's logit enters every normaliser but never the gap, and the
+    decisions follow: nothing clears tau1, so the most confident masked
+    position is drafted (Eq. 1); s < tau2 re-masks (Eq. 3)."""
+    V, mask, lb = 16, 15, 2
+    z = np.zeros((1, 2 * lb, V))
+    z[0, 0, 3], z[0, 0, 7], z[0, 0, mask] = 2.0, 1.0, 5.0   # position 0 (masked): current row
+    z[0, 1, 9] = 1.5                                         # position 1: current row
+    z[0, lb + 1, 4] = 3.0                                    # position 1 holds id 4: shadow row
+    cur = np.array([[mask, 4]])
+    tau1, tau2 = 0.05, 0.9
+    r = E.decide(z, cur, mask, tau1, tau2)
+    e = math.exp
+    s0 = e(2) + e(1) + e(5) + (V - 3)          # three non-zero logits, the rest e^0
+    conf0, gap0 = e(2) / s0, (e(2) - e(1)) / s0
+    s1 = e(3) / (e(3) + V - 1)
+    gap1 = (e(1.5) - 1.0) / (e(1.5) + V - 1)
+    assert r["yhat"][0, 0] == 3
+    assert math.isclose(r["conf"][0, 0], conf0, rel_tol=1e-12)
+    assert math.isclose(r["margin"][0, 0], abs(conf0 - tau1), rel_tol=1e-12)
+    assert math.isclose(r["gap"][0, 0], gap0, rel_tol=1e-12)
+    assert math.isclose(r["s"][0, 1], s1, rel_tol=1e-12)
+    assert math.isclose(r["margin"][0, 1], abs(s1 - tau2), rel_tol=1e-12)
+    assert math.isclose(r["gap"][0, 1], gap1, rel_tol=1e-12)
+    assert r["flags"][0].tolist() == [W.FORCED, W.REMASK]
+    assert r["tokens"][0].tolist() == [3, mask]
+    # a confidence exactly at tau1 has margin 0: never robust at any margin
+    r2 = E.decide(z, cur, mask, float(r["conf"][0, 0]), tau2)
+    assert r2["margin"][0, 0] == 0.0
+
+
+def test_step_margins_equal_the_epilogue_on_its_own_logits(tiny_weights):
+    """The model-driven step reports the same confidences, verify
+    probabilities, margins, top-2 gaps and decisions as the epilogue oracle
+    (pinned above by closed forms) applied to that step's current and shadow
+    logits: one definition of the compared positions for every parity test."""
+    cfg = tiny_cfg()
+    p, g, lb = 8, 16, 8
+    rng = np.random.default_rng(3)
+    tok = np.concatenate([wi.prompts(cfg, 1, p, seed=5)[0].numpy(), np.full(g, cfg.mask_id)])
+    tok[p + rng.choice(lb, 3, replace=False)] = rng.integers(0, cfg.mask_id, 3)   # some drafted ids
+    for tau1, tau2 in ((0.7, 0.9), (0.05, 0.5)):
+        prm = W.Params(p, g, lb, cfg.mask_id, tau1=tau1, tau2=tau2)
+        r = W.step(W.ModelProvider(tiny_weights, cfg), tok, prm, 0, 0)
+        z = np.concatenate([r.z_cur, r.z_shad])[None]
+        e = E.decide(z, tok[None, p:p + lb], cfg.mask_id, tau1, tau2)
+        masked = tok[p:p + lb] == cfg.mask_id
+        np.testing.assert_array_equal(r.flags, e["flags"][0])
+        np.testing.assert_array_equal(r.tokens[p:p + lb], e["tokens"][0])
+        np.testing.assert_allclose(r.margin, e["margin"][0], rtol=0, atol=1e-15)
+        np.testing.assert_allclose(r.top2_gap, e["gap"][0], rtol=0, atol=1e-15)
+        np.testing.assert_allclose(r.conf[masked], e["conf"][0][masked], rtol=0, atol=1e-15)
+        np.testing.assert_allclose(r.s[~masked], e["s"][0][~masked], rtol=0, atol=1e-15)
+
+
 def test_epilogue_single_peak_closed_form():
     """Rows that are zero except one peak of height h have p(peak) =
     e^h / (e^h + V - 1): the draft reads the current row, the verify the
