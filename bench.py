@@ -603,6 +603,13 @@ def main():
         line["cpu_baseline"] = {"value": head["steps_per_s"], "unit": "steps/s", "cores": hc["blas_threads"],
                                 "kind": "oracle", "sample": head["sample"],
                                 "cpus_available": hc["cpus_available"], "cpu_model": hc["cpu_model"]}
+        # oracle tokens/s at the GPU decode's step counts (extrapolated: the
+        # oracle ran one step, not the decode)
+        for key, dec in (("bs16", (line.get("decode") if a.config == "bs16" else None)),
+                         ("bs1", (line.get("bs1") or {}).get("decode"))):
+            if dec and key in cb and dec.get("forwards"):
+                _, Bk, _, gk, _, _, _, _ = CONFIGS[key]
+                cb[key]["tokens_per_s_extrapolated"] = round(Bk * gk / (dec["forwards"] / cb[key]["steps_per_s"]), 5)
         line["cpu_baselines"] = cb
     if "configs" in parts:
         del weights
