@@ -281,16 +281,26 @@ def test_resume_skips_blocks_without_masks(P):
 
 
 # ---------------------------------------------------------------- standalone epilogue
-@pytest.mark.parametrize("B,lb,V,heights", [(2, 8, 4096, (10.0, 16.0)), (8, 32, 126464, (10.0, 16.0)),
-                                            (8, 32, 126464, (0.0, 12.0)), (3, 5, 1000, (0.0, 14.0))])
-def test_epilogue_contract(P, B, lb, V, heights):
+@pytest.mark.parametrize("B,lb,V,heights,mask", [(2, 8, 4096, (10.0, 16.0), 4095),
+                                                 (8, 32, 126464, (10.0, 16.0), 126463),
+                                                 (8, 32, 126464, (0.0, 12.0), 126463),
+                                                 (3, 5, 1000, (0.0, 14.0), 999),
+                                                 # the mask id inside a chunk (another thread's
+                                                 # registers, not the vocabulary's end) and first
+                                                 (8, 32, 126464, (0.0, 12.0), 50001),
+                                                 (2, 8, 4096, (0.0, 12.0), 0)])
+def test_epilogue_contract(P, B, lb, V, heights, mask):
     """The standalone epilogue on given bf16 logits: exact statistics (bf16
     inputs are exact in fp32: max and argmax equal, the sum of exponentials to
-    1e-5) and decisions bit-exact against the float64 oracle at margin 1e-3."""
+    1e-5) and decisions bit-exact against the float64 oracle at margin 1e-3,
+    with the mask id at the vocabulary's end, inside it and first."""
     from helpers import STATS_DT, decided_mask
     from oracle import epilogue as E
-    mask = V - 1 if V != 126464 else 126463
     logits, cur, _ = wi.epilogue_inputs(B, lb, V, mask, seed=2, heights=heights, device="cuda")
+    if mask != V - 1:
+        # every other row's largest logit at the mask id: it counts in the max
+        # and the normaliser, never as the draft or the argmax
+        logits[:, ::2, mask] = 14.0
     cur0 = cur.cpu().numpy()
     prm = P.make_params(B, 1, lb, lb, mask, 0.7, 0.9)
     ws = torch.zeros(P.wino_epilogue_workspace_bytes(B, lb, V), dtype=torch.uint8, device="cuda")
