@@ -60,7 +60,17 @@ def tiny(variant="wide", seed=0, gain_std=0.1, **kw):
     Zipf bias (every block drafts in one step at tau1 = 0.7); 'wide': LM head
     std sqrt(0.5/sqrt(d)); 'sharp': backbone std 0.1 (position-dependent
     attention), wide LM head and a Zipf bias of scale 2, on which WINO drafts,
-    re-masks and re-drafts within a block (the iterating workload)."""
+    re-masks and re-drafts within a block (the iterating workload); 'midmask':
+    the wide model with mask id 1000 and the largest LM-head bias on it."""
+    if variant == "midmask":
+        # the mask id inside the vocabulary, with the largest LM-head bias:
+        # it holds the maximum of most logits rows, which counts in every
+        # normaliser but never as a draft
+        cfg = wi.preset("tiny", mask_id=1000, **kw)
+        w = wi.model_weights(cfg, seed=seed, lm_head_std=wi.wide_lm_head_std(cfg), gain_std=gain_std)
+        w["lm_bias"] = w["lm_bias"].clone()
+        w["lm_bias"][cfg.mask_id] = float(w["lm_bias"].max()) + 2.0
+        return cfg, w
     cfg = wi.preset("tiny", **kw)
     if variant == "sharp":
         return cfg, wi.model_weights(cfg, seed=seed, std=0.1, lm_head_std=wi.wide_lm_head_std(cfg),
