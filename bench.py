@@ -1,7 +1,7 @@
 """Benchmark of one WINO decoding step at the LLaDA-8B shape on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config bs16|bs1|mmada|tiny]
-                    [--parts step,bs1,epilogue,baselines,wide,configs,cpu]
+                    [--parts step,bs1,epilogue,baselines,wide,fp16,configs,cpu]
 
 A "step" is one pass of the whole hot path through the C ABI (wino_step):
 embedding, 32 layers of bidirectional attention with the shadow block and
@@ -15,8 +15,9 @@ One JSON line is printed.  `value` is steps/s over K steps timed with no
 profiling; the dominant kernel's roofline figures come from HIP events around
 its launches in a second timed pass of K steps.  The line also carries
 generated tokens/s of full decodes (literal init, and a labelled wide-init
-decode with its re-masks), the HBM-bound kernels' bandwidth, the other
-workloads, and the float64 CPU oracle timed per workload on this host.
+decode with its re-masks), the HBM-bound kernels' bandwidth, the same steps
+with fp16 activations, the other workloads, and the float64 CPU oracle timed
+per workload on this host.
 """
 from __future__ import annotations
 
@@ -101,7 +102,7 @@ def timed_steps(model, P, one_step, steps, profile_mask=0):
     return elapsed, prof
 
 
-def run_workload(P, wi, cfg, weights, name, steps, warmup, profile_dominant=True, decode=True):
+def run_workload(P, wi, cfg, weights, name, steps, warmup, profile_dominant=True, decode=True, act=0):
     """The WINO step of workload `name` from a fixed mid-block state: warmup,
     then `steps` timed steps with no profiling (the reported rate), then the
     same number of steps with HIP events around every launch of the dominant
@@ -110,7 +111,7 @@ def run_workload(P, wi, cfg, weights, name, steps, warmup, profile_dominant=True
     from the prompt (tokens/s) and its replay with counts."""
     import torch
     preset, B, p, g, lb, tau1, tau2, img = CONFIGS[name]
-    model = P.WinoModel(cfg, weights, B, p + g + lb)
+    model = P.WinoModel(cfg, weights, B, p + g + lb, act_precision=act)
     prm = P.make_params(B, p, g, lb, cfg.mask_id, tau1, tau2)
     tok0, bs0 = make_state(wi, cfg, B, p, g, lb, img)
     tok0, bs0 = tok0.cuda(), bs0.cuda()
@@ -494,7 +495,7 @@ def step_floor(r, ms):
             "frac_of_mfma_floor": round(r["step_flops"] / (PEAK_BF16_TFLOPS * 1e12) * 1e3 / ms, 4)}
 
 
-PARTS = ("step", "bs1", "epilogue", "baselines", "wide", "configs", "cpu")
+PARTS = ("step", "bs1", "epilogue", "baselines", "wide", "fp16", "configs", "cpu")
 
 
 def main():
@@ -595,6 +596,18 @@ def main():
     if "wide" in parts:
         log("wide-init decode (bs1)")
         line["wide_decode"] = run_wide(P, wi, cfg, weights, "bs1")
+    if "fp16" in parts:
+        log("fp16 activations (bs16, bs1)")
+        f16 = {"note": "the same steps with fp16 activations and fp16 copies of the weight matrices "
+                       "(act_precision = WINO_ACT_FP16); the headline value is bf16"}
+        for name in ("bs16", "bs1"):
+            r = run_workload(P, wi, cfg, weights, name, a.steps, a.warmup, decode=False, act=P.ACT_FP16)
+            ms_f = r["elapsed"] / a.steps * 1e3
+            gu = r["kernels"].get(DOMINANT, {})
+            f16[name] = {"ms_per_step": round(ms_f, 3), "steps_per_s": round(1e3 / ms_f, 4),
+                         "gemm_gateup_tflops": gu.get("tflops"),
+                         "attention_ms_per_step": r["kernels"].get("attention", {}).get("ms_per_step")}
+        line["fp16"] = f16
     if "cpu" in parts:
         log("cpu baselines (oracle)")
         cb = cpu_baselines(wi, weights)

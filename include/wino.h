@@ -54,12 +54,27 @@ typedef enum {
 
 typedef struct wino_ctx wino_ctx;
 
+/* Activation types (wino_model_config.act_precision). */
+#define WINO_ACT_BF16 0 /* bf16 activations, the weights as given (default)   */
+#define WINO_ACT_FP16 1 /* fp16 activations and fp16 copies of the matrices   */
+
 /* Backbone shape.  Requirements: d_model == n_heads*head_dim; head_dim is 64
- * or 128; d_model and d_ff are multiples of 64; vocab is a multiple of 64. */
+ * or 128; d_model and d_ff are multiples of 64; vocab is a multiple of 256.
+ * act_precision: the 16-bit type of the activations the matrix cores read
+ * (normed rows, q/k/v, attention probabilities and output, the SwiGLU
+ * product), accumulation being fp32 and the residual stream fp32 either way.
+ * WINO_ACT_FP16 keeps three more mantissa bits, so the decision probabilities
+ * move several times less from exact arithmetic (for callers whose
+ * confidences sit near a threshold), at the cost of fp16 copies of every
+ * weight matrix (2 bytes per parameter of the QKV, O, gate/up, down and LM
+ * head matrices, allocated by wino_create beside the workspace) and of fp16
+ * matrix-core throughput; activations must stay within fp16's range
+ * (|x| < 65504).  Zero-initialised configurations get WINO_ACT_BF16. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, head_dim, d_ff, vocab;
   float rope_theta; /* rotate-half RoPE base                         */
   float rms_eps;    /* RMSNorm epsilon                               */
+  int32_t act_precision; /* WINO_ACT_BF16 or WINO_ACT_FP16           */
 } wino_model_config;
 
 /* Weights, all bf16 device memory, row-major, one row per output feature.

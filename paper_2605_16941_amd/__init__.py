@@ -19,17 +19,19 @@ from ._abi import (WinoError, make_params, wino_create, wino_debug_forward, wino
                    wino_profile, wino_profile_read, wino_row_losses, wino_status_string, wino_step,
                    wino_workspace_bytes)
 
-__all__ = ["WinoModel", "WinoError", "make_params", "wino_create", "wino_destroy", "wino_step",
+ACT_BF16, ACT_FP16 = _abi.ACT_BF16, _abi.ACT_FP16
+
+__all__ = ["WinoModel", "WinoError", "make_params", "ACT_BF16", "ACT_FP16", "wino_create", "wino_destroy", "wino_step",
            "wino_decode_block", "wino_decode", "wino_epilogue", "wino_epilogue_noalloc", "wino_epilogue_workspace_bytes",
            "wino_debug_logits", "wino_debug_forward", "wino_debug_gemm", "wino_profile", "wino_profile_read",
            "wino_kernel_class_name", "wino_status_string", "wino_last_error",
            "wino_row_losses", "wino_workspace_bytes"]
 
 
-def model_config(cfg) -> _abi.wino_model_config:
+def model_config(cfg, act_precision: int = _abi.ACT_BF16) -> _abi.wino_model_config:
     """C config from any object with the backbone fields (e.g. a preset)."""
     return _abi.wino_model_config(cfg.n_layers, cfg.d_model, cfg.n_heads, cfg.head_dim, cfg.d_ff,
-                                  cfg.vocab, float(cfg.rope_theta), float(cfg.rms_eps))
+                                  cfg.vocab, float(cfg.rope_theta), float(cfg.rms_eps), act_precision)
 
 
 class WinoModel:
@@ -38,12 +40,15 @@ class WinoModel:
     ``weights`` is a dict: tok_emb [V,d], layers (list of dicts with attn_norm,
     w_qkv, w_o, ffn_norm, w_gate_up, w_down), final_norm, lm_head [V,d] and
     lm_bias (fp32 [V] or None).  The tensors must stay alive with the model.
+    ``act_precision``: ACT_BF16 (default) or ACT_FP16 (fp16 activations; the
+    context then also holds fp16 copies of the weight matrices).
     """
 
-    def __init__(self, cfg, weights: dict, max_batch: int, max_seq: int):
+    def __init__(self, cfg, weights: dict, max_batch: int, max_seq: int,
+                 act_precision: int = _abi.ACT_BF16):
         import torch
         self.cfg = cfg
-        self.ccfg = model_config(cfg)
+        self.ccfg = model_config(cfg, act_precision)
         self.weights = weights
         n = cfg.n_layers
 

@@ -44,7 +44,10 @@ STATUS = {0: "WINO_OK", -1: "WINO_ERR_INVALID_ARG", -2: "WINO_ERR_SHAPE", -3: "W
 class wino_model_config(C.Structure):
     _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_heads", C.c_int32),
                 ("head_dim", C.c_int32), ("d_ff", C.c_int32), ("vocab", C.c_int32),
-                ("rope_theta", C.c_float), ("rms_eps", C.c_float)]
+                ("rope_theta", C.c_float), ("rms_eps", C.c_float), ("act_precision", C.c_int32)]
+
+
+ACT_BF16, ACT_FP16 = 0, 1
 
 
 class wino_weights(C.Structure):

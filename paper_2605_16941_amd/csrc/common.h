@@ -50,6 +50,38 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Activation element types of the matrix-core operands (activations and the
+// weights they multiply): bf16, or fp16 for three more mantissa bits where
+// decisions near a threshold need them.  Storage is 16-bit either way;
+// conversions round to nearest even; accumulation is fp32.
+typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
+typedef __attribute__((__vector_size__(2 * sizeof(_Float16)))) _Float16 f16x2;
+struct ActBf16 {
+  typedef bf16x8 v8;
+  static constexpr bool kF16 = false;
+  __device__ static __forceinline__ v8 frag(const uint4& v) { return __builtin_bit_cast(bf16x8, v); }
+  __device__ static __forceinline__ f32x16 mma(const v8& a, const v8& b, const f32x16& c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ uint32_t pack2(float lo, float hi) { return pack2bf(lo, hi); }
+  __device__ static __forceinline__ uint16_t cvt(float f) { return f2bf(f); }
+  __device__ static __forceinline__ float val(uint16_t v) { return bf2f(v); }
+};
+struct ActF16 {
+  typedef f16x8 v8;
+  static constexpr bool kF16 = true;
+  __device__ static __forceinline__ v8 frag(const uint4& v) { return __builtin_bit_cast(f16x8, v); }
+  __device__ static __forceinline__ f32x16 mma(const v8& a, const v8& b, const f32x16& c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ uint32_t pack2(float lo, float hi) {
+    const f16x2 v = {(_Float16)lo, (_Float16)hi};
+    return __builtin_bit_cast(uint32_t, v);
+  }
+  __device__ static __forceinline__ uint16_t cvt(float f) { return __builtin_bit_cast(uint16_t, (_Float16)f); }
+  __device__ static __forceinline__ float val(uint16_t v) { return (float)__builtin_bit_cast(_Float16, v); }
+};
+
 // Reductions on the vector ALU alone, without the LDS round trip of a
 // shuffle per step: DPP lane swaps inside quads (xor 1, xor 2), the half-row
 // and row mirrors (groups of 8 and 16 lanes), then rows 0<->1 and 2<->3

@@ -5,13 +5,14 @@
 // [0, T) except y_cur,j at c0+j - including all shadow rows and itself.
 // No causal mask and no cache: every step recomputes all rows.
 //
-// Layout: q, k bf16 [B, H, Tp, hd] (RoPE already applied), v transposed
-// [B, H, hd, Tp]; output o bf16 [B*T, H*hd] row-major.
+// Layout: q, k [B, H, Tp, hd] (RoPE already applied), v transposed
+// [B, H, hd, Tp]; output o [B*T, H*hd] row-major; all in the activation type
+// A (bf16 or fp16), whose MFMA form the kernel uses.
 //
 // Each wave owns 32 query rows.  Scores are computed transposed, S^T = K Q^T
 // (32x32x16 MFMA), so a lane holds 32 keys of ONE query row and the online
 // softmax max / sum stay inside the lane (plus its partner lane 32 apart).
-// The same registers, rounded to bf16, are the B operand of O^T = V^T P^T
+// The same registers, rounded to A, are the B operand of O^T = V^T P^T
 // (the softmax and its running sum stay in fp32).
 //
 // K and V^T tiles of 64 keys stream global -> LDS by LDS-DMA into two stages
@@ -41,7 +42,7 @@ __device__ __forceinline__ int perm_key(int r) {
 // CQ (compact queries): only each sequence's current-block rows and shadow
 // rows are queried - compact query i < Lb is row c0 + i, i >= Lb is row
 // S + i - Lb - and output row i of sequence b goes to o row b*(Lb+Ls) + i.
-template <int HD, int NW, bool CQ, int NS>
+template <int HD, int NW, bool CQ, int NS, class A>
 __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const uint16_t* __restrict__ q,
                                                        const uint16_t* __restrict__ k,
                                                        const uint16_t* __restrict__ vt, int H,
@@ -53,7 +54,7 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
   constexpr int K_INS = BKV / KROWS / NW;  // K DMA instructions per wave
   constexpr int V_INS = HD / 8 / NW;       // V^T DMA instructions per wave (8 rows each)
   static_assert(K_INS * KROWS * NW == BKV && V_INS * 8 * NW == HD, "loader split");
-  constexpr int KTILE = BKV * HD;    // bf16 elements
+  constexpr int KTILE = BKV * HD;    // 16-bit elements
   constexpr int STAGE = 2 * KTILE;   // K tile then V^T tile
   static_assert(NS >= 2, "pipeline stages");
   __shared__ __attribute__((aligned(1024))) uint16_t smem[NS * STAGE];
@@ -116,12 +117,12 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
       dma16(vsrc[i] + kv0 - (i & 3) * 512, sV + (wave * V_INS + (i & ~3)) * 512, i & 3);
   };
 
-  bf16x8 qf[KS];
+  typename A::v8 qf[KS];
   {
     const int qrow = qvalid && myq < g.T ? myq : g.T - 1;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
-      qf[ks] = as_bf16x8(*reinterpret_cast<const uint4*>(qb + (size_t)qrow * HD + ks * 16 + grp * 8));
+      qf[ks] = A::frag(*reinterpret_cast<const uint4*>(qb + (size_t)qrow * HD + ks * 16 + grp * 8));
   }
 
   f32x16 oacc[FE];
@@ -178,9 +179,9 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
     auto vfrag = [&](int ks4, int fe) {
       const int row = fe * 32 + (lane & 31);
       const int ch = (ks4 * 2 + grp) ^ vswz[fe];
-      return as_bf16x8(*reinterpret_cast<const uint4*>(sV + row * BKV + ch * 8));
+      return A::frag(*reinterpret_cast<const uint4*>(sV + row * BKV + ch * 8));
     };
-    bf16x8 vf[2][FE];
+    typename A::v8 vf[2][FE];
     f32x16 s[2];
 #pragma unroll
     for (int kb2 = 0; kb2 < 2; ++kb2)
@@ -188,9 +189,9 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
       for (int i = 0; i < 16; ++i) s[kb2][i] = 0.f;
     auto kfrag = [&](int ks, int kb2) {
       const int ch = (ks * 2 + grp) ^ kswz[kb2];
-      return as_bf16x8(*reinterpret_cast<const uint4*>(sK + (kb2 * 32 + kr) * HD + ch * 8));
+      return A::frag(*reinterpret_cast<const uint4*>(sK + (kb2 * 32 + kr) * HD + ch * 8));
     };
-    bf16x8 kf[3][2];
+    typename A::v8 kf[3][2];
     kf[0][0] = kfrag(0, 0);
     kf[0][1] = kfrag(0, 1);
     kf[1][0] = kfrag(1, 0);
@@ -205,8 +206,8 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
         kf[(ks + 2) % 3][1] = kfrag(ks + 2, 1);
         __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
       }
-      s[0] = mfma32(kf[ks % 3][0], qf[ks], s[0]);
-      s[1] = mfma32(kf[ks % 3][1], qf[ks], s[1]);
+      s[0] = A::mma(kf[ks % 3][0], qf[ks], s[0]);
+      s[1] = A::mma(kf[ks % 3][1], qf[ks], s[1]);
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 1);
     }
     // the first V^T fragments load while the softmax runs
@@ -270,16 +271,16 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
 #pragma unroll
         for (int fe = 0; fe < FE; ++fe) vf[(ks4 + 1) & 1][fe] = vfrag(ks4 + 1, fe);
       }
-      // P in bf16: registers 8*(ks4&1)..+7 of block ks4/2 hold keys
+      // P in A (values up to 2^8): registers 8*(ks4&1)..+7 of block ks4/2 hold keys
       // 16*ks4 + 8*grp + 0..7.
       const int base = 8 * (ks4 & 1);
       uint32_t ph[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        ph[e] = pack2bf(s[ks4 >> 1][base + 2 * e], s[ks4 >> 1][base + 2 * e + 1]);
-      const bf16x8 pf = as_bf16x8(make_uint4(ph[0], ph[1], ph[2], ph[3]));
+        ph[e] = A::pack2(s[ks4 >> 1][base + 2 * e], s[ks4 >> 1][base + 2 * e + 1]);
+      const typename A::v8 pf = A::frag(make_uint4(ph[0], ph[1], ph[2], ph[3]));
 #pragma unroll
-      for (int fe = 0; fe < FE; ++fe) oacc[fe] = mfma32(vf[ks4 & 1][fe], pf, oacc[fe]);
+      for (int fe = 0; fe < FE; ++fe) oacc[fe] = A::mma(vf[ks4 & 1][fe], pf, oacc[fe]);
     }
   }
 
@@ -294,14 +295,14 @@ __global__ __launch_bounds__(NW * 64, 8 / NW) void attn_kernel(StepGeom g, const
       for (int i = 0; i < 16; i += 4) {
         // rows 8*(i/4) + 4*grp + 0..3 of this e block: 4 consecutive outputs
         uint2 w;
-        w.x = pack2bf(oacc[fe][i] * inv, oacc[fe][i + 1] * inv);
-        w.y = pack2bf(oacc[fe][i + 2] * inv, oacc[fe][i + 3] * inv);
+        w.x = A::pack2(oacc[fe][i] * inv, oacc[fe][i + 1] * inv);
+        w.y = A::pack2(oacc[fe][i + 2] * inv, oacc[fe][i + 3] * inv);
         *reinterpret_cast<uint2*>(dst + fe * 32 + mfma_row(i, lane)) = w;
       }
   }
 }
 
-template <int HD>
+template <int HD, class A>
 hipError_t launch_hd(const StepGeom& g, const uint16_t* q, const uint16_t* k, const uint16_t* vt,
                      int H, uint16_t* o, float scale_log2, bool compact, hipStream_t st) {
   if (compact) {
@@ -309,7 +310,7 @@ hipError_t launch_hd(const StepGeom& g, const uint16_t* q, const uint16_t* k, co
     // 48 against 58 us at 2112 rows and batch 4, for 64 compact queries per
     // sequence; the two idle waves only copy tiles)
     dim3 grid((g.Lb + g.Ls + 127) / 128, H, g.B);
-    attn_kernel<HD, 4, true, 2><<<grid, 256, 0, st>>>(g, q, k, vt, H, o, scale_log2);
+    attn_kernel<HD, 4, true, 2, A><<<grid, 256, 0, st>>>(g, q, k, vt, H, o, scale_log2);
     return hipGetLastError();
   }
   // 128-query workgroups (four waves) at every size: at 544 rows they take
@@ -317,7 +318,7 @@ hipError_t launch_hd(const StepGeom& g, const uint16_t* q, const uint16_t* k, co
   // two-wave kernel spends 96 accumulation registers and runs one wave per
   // SIMD), and three or four K/V stages did not pay there either.
   dim3 grid((g.T + 127) / 128, H, g.B);
-  attn_kernel<HD, 4, false, 2><<<grid, 256, 0, st>>>(g, q, k, vt, H, o, scale_log2);
+  attn_kernel<HD, 4, false, 2, A><<<grid, 256, 0, st>>>(g, q, k, vt, H, o, scale_log2);
   return hipGetLastError();
 }
 
@@ -327,8 +328,13 @@ hipError_t launch_attention(const StepGeom& g, const uint16_t* q, const uint16_t
                             const uint16_t* vt, int H, int hd, uint16_t* o, hipStream_t st,
                             bool compact) {
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
-  if (hd == 128) return launch_hd<128>(g, q, k, vt, H, o, scale_log2, compact, st);
-  if (hd == 64) return launch_hd<64>(g, q, k, vt, H, o, scale_log2, compact, st);
+  if (g.f16) {
+    if (hd == 128) return launch_hd<128, ActF16>(g, q, k, vt, H, o, scale_log2, compact, st);
+    if (hd == 64) return launch_hd<64, ActF16>(g, q, k, vt, H, o, scale_log2, compact, st);
+  } else {
+    if (hd == 128) return launch_hd<128, ActBf16>(g, q, k, vt, H, o, scale_log2, compact, st);
+    if (hd == 64) return launch_hd<64, ActBf16>(g, q, k, vt, H, o, scale_log2, compact, st);
+  }
   return hipErrorInvalidValue;
 }
 

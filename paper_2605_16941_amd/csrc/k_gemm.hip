@@ -1,5 +1,6 @@
-// bf16 GEMM C = A * W^T on gfx950 matrix cores (v_mfma_f32_32x32x16_bf16),
-// with the epilogues of the WINO forward fused in:
+// GEMM C = A * W^T on gfx950 matrix cores (v_mfma_f32_32x32x16_bf16, or the
+// _f16 form when activations and weights are fp16), with the epilogues of the
+// WINO forward fused in:
 //   QKV projection + rotate-half RoPE at the WINO position ids,
 //   residual add into the fp32 stream (O projection, FFN down projection),
 //   SwiGLU of interleaved gate/up tiles,
@@ -7,9 +8,9 @@
 //   logit of the current token) so the logits never reach memory,
 //   plain fp32 store (+bias) for the test entry point.
 //
-// The LM-head epilogues read the final hidden rows as two bf16 parts (hi and
+// The LM-head epilogues read the final hidden rows as two 16-bit parts (hi and
 // lo of the fp32 value) and multiply both with the same W tile, so the logits
-// carry ~16 mantissa bits of the hidden state instead of bf16's 8.
+// carry ~16 (bf16) or ~22 (fp16) mantissa bits of the hidden state.
 //
 // Tiling: a workgroup owns a BM x BN output tile and walks K in steps of 64.
 // A and W tiles go straight from global memory into LDS (gfx950 LDS-DMA,
@@ -165,7 +166,7 @@ __device__ __forceinline__ void epi_partial(const GemmCall& c, f32x16 (&acc)[FM]
 // goes in a scalar register, the lane's column in the vector offset.  In a
 // tile that crosses the last row, rows past it get an offset beyond the
 // buffer range, which drops their stores.
-template <int FM, int FN>
+template <class A, int FM, int FN>
 __device__ __forceinline__ void epi_swiglu(const GemmCall& c, f32x16 (&acc)[FM][FN], int rowb,
                                            int colb, int lane) {
   constexpr int H2 = FN / 2, WTM = FM * 32;
@@ -190,7 +191,7 @@ __device__ __forceinline__ void epi_swiglu(const GemmCall& c, f32x16 (&acc)[FM][
         for (int fn = 0; fn < H2; ++fn) {
           const float g = acc[fm][fn][i], u = acc[fm][fn + H2][i];
           const float sg = __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(g * -1.44269504088896341f));
-          __builtin_amdgcn_raw_buffer_store_b16(f2bf(g * u * sg), rs, vo + fn * 64, srow * ld2, 0);
+          __builtin_amdgcn_raw_buffer_store_b16(A::cvt(g * u * sg), rs, vo + fn * 64, srow * ld2, 0);
         }
       }
   };
@@ -231,7 +232,7 @@ struct TileRows {
 // MFMA layout would scatter 2-byte writes over hd rows of the transposed
 // buffer.  16-byte chunks are XOR-swizzled by the row index, so the
 // half-waves' writes (4 rows apart) land in distinct banks.
-template <int FM, int FN, bool TWO>
+template <class A, int FM, int FN, bool TWO>
 __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM][FN], int rowb,
                                              int colb, int lane, uint16_t* ws) {
   constexpr int H2 = FN / 2;
@@ -288,7 +289,7 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
           const float x1 = acc[fm][fn][i], x2 = acc[fm][fn + 2][i];
           const float r1 = fmaf(x1, cs, -(x2 * sn));  // element e
           const float r2 = fmaf(x2, cs, x1 * sn);     // element e + hd/2
-          const uint32_t pk = pack2bf(r1, r2);
+          const uint32_t pk = A::pack2(r1, r2);
           uint16_t* row = wl + lrc * HD + (((((fn ^ g4) << 2) | (q8 ^ i3))) << 3);
           row[c8 << 3] = (uint16_t)pk;
           row[(c8 ^ 8) << 3] = (uint16_t)(pk >> 16);
@@ -340,7 +341,7 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
           // (lane ^ 1 by a DPP quad swap, no LDS round trip)
           const float got = __uint_as_float(dpp_mov<0xB1>(__float_as_uint(odd ? r1 : r2)));
           const int ee = odd ? e + half - 1 : e;
-          const uint32_t pk = odd ? pack2bf(got, r2) : pack2bf(r1, got);
+          const uint32_t pk = odd ? A::pack2(got, r2) : A::pack2(r1, got);
           *reinterpret_cast<uint32_t*>(wr + (((ee >> 3) ^ sw) << 3) + (ee & 7)) = pk;
         }
       }
@@ -391,8 +392,8 @@ __device__ __forceinline__ void epi_qkv_rope(const GemmCall& c, f32x16 (&acc)[FM
         for (int q = 0; q < 4; ++q) {
           const int tl = fm * 32 + 8 * q + 4 * (lane >> 5);
           uint2 v;
-          v.x = pack2bf(acc[fm][fn][4 * q], acc[fm][fn][4 * q + 1]);
-          v.y = pack2bf(acc[fm][fn][4 * q + 2], acc[fm][fn][4 * q + 3]);
+          v.x = A::pack2(acc[fm][fn][4 * q], acc[fm][fn][4 * q + 1]);
+          v.y = A::pack2(acc[fm][fn][4 * q + 2], acc[fm][fn][4 * q + 3]);
           const int slot = (tl >> 2) ^ ((e >> 1) & SMASK);
           *reinterpret_cast<uint2*>(wr + slot * 4) = v;
         }
@@ -558,7 +559,7 @@ __device__ __forceinline__ int lds_swz(int r) {
 // tiles XW more LDS stages than the two of A, so W copies have 1 + XW K
 // steps to land instead of one (for weights that few row tiles share, whose
 // copies mostly miss L2).
-template <int BM, int BN, int WM, int WN, int EPI, int KB, int NST, int OCC, int XW>
+template <int BM, int BN, int WM, int WN, int EPI, int KB, int NST, int OCC, int XW, class A>
 __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_kernel(const GemmCall c) {
   static_assert(KB == 32 || KB == 64, "K step");
   static_assert(NST >= 2, "pipeline stages");
@@ -691,7 +692,7 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
   }
   constexpr int KS = KB / 16;
   static_assert(KS % 2 == 0, "fragment buffers alternate per step");
-  bf16x8 af[2][FM], bf[2][FN], al[2][SPLIT ? FM : 1];
+  typename A::v8 af[2][FM], bf[2][FN], al[2][SPLIT ? FM : 1];
 
   // The K loop for a wave whose first FMV of its FM 32-row blocks hold rows
   // below M (FMV = FM everywhere but in a partial last row tile): the other
@@ -708,16 +709,16 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
     const int kc = ks * 2 + (lane >> 5);
 #pragma unroll
     for (int fm = 0; fm < FMV; ++fm)
-      af[buf][fm] = as_bf16x8(*reinterpret_cast<const uint4*>(
+      af[buf][fm] = A::frag(*reinterpret_cast<const uint4*>(
           sA + (arow + fm * 32) * KB + ((kc ^ aswz[fm]) << 3)));
 #pragma unroll
     for (int fn = 0; fn < FN; ++fn)
-      bf[buf][fn] = as_bf16x8(*reinterpret_cast<const uint4*>(
+      bf[buf][fn] = A::frag(*reinterpret_cast<const uint4*>(
           sB + (brow + fn * 32) * KB + ((kc ^ bswz[fn]) << 3)));
     if constexpr (SPLIT) {
 #pragma unroll
       for (int fm = 0; fm < FMV; ++fm)
-        al[buf][fm] = as_bf16x8(*reinterpret_cast<const uint4*>(
+        al[buf][fm] = A::frag(*reinterpret_cast<const uint4*>(
             sA + (BM + arow + fm * 32) * KB + ((kc ^ alswz[fm]) << 3)));
     }
     }
@@ -726,12 +727,12 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
 #pragma unroll
     for (int fm = 0; fm < FMV; ++fm)
 #pragma unroll
-      for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma32(af[buf][fm], bf[buf][fn], acc[fm][fn]);
+      for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = A::mma(af[buf][fm], bf[buf][fn], acc[fm][fn]);
     if constexpr (SPLIT) {
 #pragma unroll
       for (int fm = 0; fm < FMV; ++fm)
 #pragma unroll
-        for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = mfma32(al[buf][fm], bf[buf][fn], acc[fm][fn]);
+        for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = A::mma(al[buf][fm], bf[buf][fn], acc[fm][fn]);
     }
   };
   // steps 0..KS-2 of a tile: the reads of step ks+1 go between the MFMAs of ks
@@ -871,12 +872,12 @@ __global__ __launch_bounds__(WM* WN * 64, (OCC * WM * WN + 3) / 4) void gemm_ker
     }
   }
   else if constexpr (EPI == EPI_STORE_F32 || EPI == EPI_LOGITS) epi_store<FM, FN>(c, acc, rowb, colb, lane);
-  else if constexpr (EPI == EPI_SWIGLU) epi_swiglu<FM, FN>(c, acc, rowb, colb, lane);
+  else if constexpr (EPI == EPI_SWIGLU) epi_swiglu<A, FM, FN>(c, acc, rowb, colb, lane);
   else if constexpr (EPI == EPI_QKV_ROPE) {
     // each wave stages its WTM x WTN tile in its own LDS region
     static_assert(BM * BN <= LDS_ELEMS, "QKV staging fits the pipeline LDS");
-    if (c.geom.T >= WTM) epi_qkv_rope<FM, FN, true>(c, acc, rowb, colb, lane, smem + wave * (WTM * WTN));
-    else epi_qkv_rope<FM, FN, false>(c, acc, rowb, colb, lane, smem + wave * (WTM * WTN));
+    if (c.geom.T >= WTM) epi_qkv_rope<A, FM, FN, true>(c, acc, rowb, colb, lane, smem + wave * (WTM * WTN));
+    else epi_qkv_rope<A, FM, FN, false>(c, acc, rowb, colb, lane, smem + wave * (WTM * WTN));
   }
   else epi_lmstats<BM, WM, WN, FM, FN>(c, acc, m0, tn, rowb, colb, lane, wm, wn, smem);
 }
@@ -1067,7 +1068,7 @@ std::mutex g_plan_mu;
 PlanEntry g_plans[32];
 int g_n_plans = 0;
 
-template <int BM, int BN, int WM, int WN, int EPI, int KB, int NST, int OCC, int XW>
+template <int BM, int BN, int WM, int WN, int EPI, int KB, int NST, int OCC, int XW, class A>
 hipError_t launch_one(const GemmCall& c, hipStream_t st) {
   constexpr bool split = EPI == EPI_LMSTATS || EPI == EPI_LOGITS;
   constexpr int arows = split ? 2 * BM : BM;
@@ -1081,24 +1082,30 @@ hipError_t launch_one(const GemmCall& c, hipStream_t st) {
       const int mainTM = c.split_row0 / BM;
       units = mainTM * nTN + (nTM - mainTM) * nTN * c.splits;
     }
-    gemm_kernel<BM, BN, WM, WN, EPI, KB, NST, OCC, XW><<<dim3(units), dim3(WM * WN * 64), 0, st>>>(c);
+    gemm_kernel<BM, BN, WM, WN, EPI, KB, NST, OCC, XW, A><<<dim3(units), dim3(WM * WN * 64), 0, st>>>(c);
     return hipGetLastError();
   } else {
     return hipErrorInvalidValue;
   }
 }
 
-template <int BM, int BN, int WM, int WN, int KB, int NST, int OCC, int XW = 0>
-hipError_t launch_cfg(const GemmCall& c, hipStream_t st) {
+template <int BM, int BN, int WM, int WN, int KB, int NST, int OCC, int XW, class A>
+hipError_t launch_cfg_t(const GemmCall& c, hipStream_t st) {
   switch (c.epi) {
-    case EPI_QKV_ROPE: return launch_one<BM, BN, WM, WN, EPI_QKV_ROPE, KB, NST, OCC, XW>(c, st);
-    case EPI_RESIDUAL: return launch_one<BM, BN, WM, WN, EPI_RESIDUAL, KB, NST, OCC, XW>(c, st);
-    case EPI_SWIGLU: return launch_one<BM, BN, WM, WN, EPI_SWIGLU, KB, NST, OCC, XW>(c, st);
-    case EPI_LMSTATS: return launch_one<BM, BN, WM, WN, EPI_LMSTATS, KB, NST, OCC, XW>(c, st);
-    case EPI_STORE_F32: return launch_one<BM, BN, WM, WN, EPI_STORE_F32, KB, NST, OCC, XW>(c, st);
-    case EPI_LOGITS: return launch_one<BM, BN, WM, WN, EPI_LOGITS, KB, NST, OCC, XW>(c, st);
+    case EPI_QKV_ROPE: return launch_one<BM, BN, WM, WN, EPI_QKV_ROPE, KB, NST, OCC, XW, A>(c, st);
+    case EPI_RESIDUAL: return launch_one<BM, BN, WM, WN, EPI_RESIDUAL, KB, NST, OCC, XW, A>(c, st);
+    case EPI_SWIGLU: return launch_one<BM, BN, WM, WN, EPI_SWIGLU, KB, NST, OCC, XW, A>(c, st);
+    case EPI_LMSTATS: return launch_one<BM, BN, WM, WN, EPI_LMSTATS, KB, NST, OCC, XW, A>(c, st);
+    case EPI_STORE_F32: return launch_one<BM, BN, WM, WN, EPI_STORE_F32, KB, NST, OCC, XW, A>(c, st);
+    case EPI_LOGITS: return launch_one<BM, BN, WM, WN, EPI_LOGITS, KB, NST, OCC, XW, A>(c, st);
   }
   return hipErrorInvalidValue;
+}
+
+template <int BM, int BN, int WM, int WN, int KB, int NST, int OCC, int XW = 0>
+hipError_t launch_cfg(const GemmCall& c, hipStream_t st) {
+  return c.f16 ? launch_cfg_t<BM, BN, WM, WN, KB, NST, OCC, XW, ActF16>(c, st)
+               : launch_cfg_t<BM, BN, WM, WN, KB, NST, OCC, XW, ActBf16>(c, st);
 }
 
 }  // namespace

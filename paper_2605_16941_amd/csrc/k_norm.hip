@@ -1,6 +1,9 @@
 // Embedding gather and RMSNorm kernels: one wave per row, the row held in
 // registers (16-byte chunks of 8 elements per lane), fp32 sum of squares by a
-// wave butterfly, bf16 output rounded to nearest even.
+// wave butterfly, output in the activation type A (bf16 or fp16) rounded to
+// nearest even.  Gains and the embedding table are bf16 weights.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -8,7 +11,7 @@ namespace wino {
 
 namespace {
 
-template <int CPL>
+template <class A, int CPL>
 __device__ __forceinline__ void norm_store(float (&v)[CPL][8], float ss, const uint16_t* gain,
                                            float eps, int d, int lane, uint16_t* out,
                                            uint16_t* out_lo = nullptr) {
@@ -27,7 +30,7 @@ __device__ __forceinline__ void norm_store(float (&v)[CPL][8], float ss, const u
       uint4 o;
       uint32_t* op = reinterpret_cast<uint32_t*>(&o);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) op[e] = pack2bf(y[2 * e], y[2 * e + 1]);
+      for (int e = 0; e < 4; ++e) op[e] = A::pack2(y[2 * e], y[2 * e + 1]);
       *reinterpret_cast<uint4*>(out + ch * 8) = o;
       if (out_lo) {
         const uint16_t* hi = reinterpret_cast<const uint16_t*>(&o);
@@ -35,14 +38,14 @@ __device__ __forceinline__ void norm_store(float (&v)[CPL][8], float ss, const u
         uint32_t* lp = reinterpret_cast<uint32_t*>(&lo);
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          lp[e] = pack2bf(y[2 * e] - bf2f(hi[2 * e]), y[2 * e + 1] - bf2f(hi[2 * e + 1]));
+          lp[e] = A::pack2(y[2 * e] - A::val(hi[2 * e]), y[2 * e + 1] - A::val(hi[2 * e + 1]));
         *reinterpret_cast<uint4*>(out_lo + ch * 8) = lo;
       }
     }
   }
 }
 
-template <int CPL>
+template <class A, int CPL>
 __global__ __launch_bounds__(256) void embed_norm_kernel(StepGeom g, const int32_t* __restrict__ tokens,
                                                          const uint16_t* __restrict__ emb, int vocab,
                                                          const uint16_t* __restrict__ gain, float eps,
@@ -78,7 +81,7 @@ __global__ __launch_bounds__(256) void embed_norm_kernel(StepGeom g, const int32
       for (int e = 0; e < 8; ++e) v[c][e] = 0.f;
     }
   }
-  norm_store<CPL>(v, ss, gain, eps, d, lane, h + (size_t)m * d);
+  norm_store<A, CPL>(v, ss, gain, eps, d, lane, h + (size_t)m * d);
 }
 
 template <int CPL>
@@ -152,7 +155,7 @@ __device__ __forceinline__ float load_row_reduce(float* xr, const float* part, i
   return ss;
 }
 
-template <int CPL>
+template <class A, int CPL>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x,
                                                       const uint16_t* __restrict__ gain, float eps,
                                                       int M, int d, uint16_t* __restrict__ h,
@@ -168,7 +171,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x,
   const bool has = m >= part_row0;
   const float ss = load_row_reduce<CPL>(x + (size_t)m * d, part + (size_t)(has ? m - part_row0 : 0) * d,
                                         has ? n_part : 0, (size_t)(M - part_row0) * d, d, lane, v);
-  norm_store<CPL>(v, ss, gain, eps, d, lane, h + (size_t)m * d);
+  norm_store<A, CPL>(v, ss, gain, eps, d, lane, h + (size_t)m * d);
 }
 
 // RMSNorm with a whole workgroup per row (d = 2048 * CPT): 256 threads hold
@@ -178,7 +181,7 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(float* __restrict__ x,
 // split-K partials when known at compile time (their loads are then all
 // issued before the first wait; -1: a runtime loop over them, one round trip
 // each), added in split order either way.
-template <int CPT, int NP>
+template <class A, int CPT, int NP>
 __global__ __launch_bounds__(256) void rmsnorm_row_kernel(float* __restrict__ x,
                                                           const uint16_t* __restrict__ gain, float eps,
                                                           int M, int d, uint16_t* __restrict__ h,
@@ -256,7 +259,7 @@ __global__ __launch_bounds__(256) void rmsnorm_row_kernel(float* __restrict__ x,
     uint32_t* op = reinterpret_cast<uint32_t*>(&o);
 #pragma unroll
     for (int e = 0; e < 4; ++e)
-      op[e] = pack2bf(v[c][2 * e] * rs * bf2f(gp[2 * e]), v[c][2 * e + 1] * rs * bf2f(gp[2 * e + 1]));
+      op[e] = A::pack2(v[c][2 * e] * rs * bf2f(gp[2 * e]), v[c][2 * e + 1] * rs * bf2f(gp[2 * e + 1]));
     *reinterpret_cast<uint4*>(out + ch * 8) = o;
   }
 }
@@ -274,7 +277,7 @@ __global__ __launch_bounds__(256) void residual_reduce_kernel(float* __restrict_
                        (size_t)(M - part_row0) * d, d, lane, v);
 }
 
-template <int CPL>
+template <class A, int CPL>
 __global__ __launch_bounds__(256) void select_norm_kernel(StepGeom g, int mode,
                                                           const int32_t* __restrict__ tokens,
                                                           const float* __restrict__ x,
@@ -310,7 +313,7 @@ __global__ __launch_bounds__(256) void select_norm_kernel(StepGeom g, int mode,
   float v[CPL][8];
   const size_t xrow = compact ? (size_t)b * (g.Lb + g.Ls) + src : (size_t)b * g.T + src;
   const float ss = load_row_f32<CPL>(x + xrow * d, d, lane, v);
-  norm_store<CPL>(v, ss, gain, eps, d, lane, hf + (size_t)r * d, hf_lo + (size_t)r * d);
+  norm_store<A, CPL>(v, ss, gain, eps, d, lane, hf + (size_t)r * d, hf_lo + (size_t)r * d);
 }
 
 // Copy of the current-block and shadow rows of every sequence (fp32).
@@ -325,47 +328,84 @@ __global__ __launch_bounds__(256) void gather_block_rows_kernel(StepGeom g, cons
   for (int c = threadIdx.x; c < d / 4; c += 256) dst[c] = src[c];
 }
 
+// Weights bf16 -> fp16 (round to nearest even), 8 elements per thread; n is
+// a multiple of 8.
+__global__ __launch_bounds__(256) void bf16_to_f16_kernel(const uint16_t* __restrict__ in,
+                                                          uint16_t* __restrict__ out, size_t n8) {
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n8; i += (size_t)gridDim.x * 256) {
+    const uint4 raw = reinterpret_cast<const uint4*>(in)[i];
+    const uint32_t* w = &raw.x;
+    uint4 o;
+    uint32_t* op = &o.x;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      op[e] = ActF16::pack2(__uint_as_float(w[e] << 16), __uint_as_float(w[e] & 0xFFFF0000u));
+    reinterpret_cast<uint4*>(out)[i] = o;
+  }
+}
+
 }  // namespace
 
+void launch_bf16_to_f16(const uint16_t* in, uint16_t* out, size_t n, hipStream_t st) {
+  const size_t n8 = n / 8;
+  if (n8 == 0) return;
+  const size_t blocks = std::min<size_t>((n8 + 255) / 256, 8192);
+  bf16_to_f16_kernel<<<blocks, 256, 0, st>>>(in, out, n8);
+}
+
 // The library accepts d <= 4096 (up to 8 chunks of 8 elements per lane).
+template <class A>
+void embed_norm_impl(const StepGeom& g, const int32_t* tokens, const uint16_t* emb, int vocab,
+                     const uint16_t* gain, float eps, int d, float* x, uint16_t* h, hipStream_t st) {
+  const int M = g.B * g.T;
+  dim3 grid((M + 3) / 4), block(256);
+  if (d <= 512) embed_norm_kernel<A, 1><<<grid, block, 0, st>>>(g, tokens, emb, vocab, gain, eps, d, x, h);
+  else if (d <= 1024) embed_norm_kernel<A, 2><<<grid, block, 0, st>>>(g, tokens, emb, vocab, gain, eps, d, x, h);
+  else if (d <= 2048) embed_norm_kernel<A, 4><<<grid, block, 0, st>>>(g, tokens, emb, vocab, gain, eps, d, x, h);
+  else embed_norm_kernel<A, 8><<<grid, block, 0, st>>>(g, tokens, emb, vocab, gain, eps, d, x, h);
+}
+
 void launch_embed_norm(const StepGeom& g, const int32_t* tokens, const uint16_t* emb, int vocab,
                        const uint16_t* gain, float eps, int d, float* x, uint16_t* h,
                        hipStream_t st) {
-  const int M = g.B * g.T;
-  dim3 grid((M + 3) / 4), block(256);
-  if (d <= 512) embed_norm_kernel<1><<<grid, block, 0, st>>>(g, tokens, emb, vocab, gain, eps, d, x, h);
-  else if (d <= 1024) embed_norm_kernel<2><<<grid, block, 0, st>>>(g, tokens, emb, vocab, gain, eps, d, x, h);
-  else if (d <= 2048) embed_norm_kernel<4><<<grid, block, 0, st>>>(g, tokens, emb, vocab, gain, eps, d, x, h);
-  else embed_norm_kernel<8><<<grid, block, 0, st>>>(g, tokens, emb, vocab, gain, eps, d, x, h);
+  if (g.f16) embed_norm_impl<ActF16>(g, tokens, emb, vocab, gain, eps, d, x, h, st);
+  else embed_norm_impl<ActBf16>(g, tokens, emb, vocab, gain, eps, d, x, h, st);
 }
 
-template <int CPT>
+template <class A, int CPT>
 void launch_row_norm(float* x, const uint16_t* gain, float eps, int M, int d, uint16_t* h,
                      const float* part, int n_part, int part_row0, hipStream_t st) {
   // the split counts the residual planner uses get their own instance
   switch (n_part) {
-    case 0: rmsnorm_row_kernel<CPT, 0><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0); break;
-    case 2: rmsnorm_row_kernel<CPT, 2><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0); break;
-    case 3: rmsnorm_row_kernel<CPT, 3><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0); break;
-    case 4: rmsnorm_row_kernel<CPT, 4><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0); break;
-    case 8: rmsnorm_row_kernel<CPT, 8><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0); break;
-    default: rmsnorm_row_kernel<CPT, -1><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
+    case 0: rmsnorm_row_kernel<A, CPT, 0><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0); break;
+    case 2: rmsnorm_row_kernel<A, CPT, 2><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0); break;
+    case 3: rmsnorm_row_kernel<A, CPT, 3><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0); break;
+    case 4: rmsnorm_row_kernel<A, CPT, 4><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0); break;
+    case 8: rmsnorm_row_kernel<A, CPT, 8><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0); break;
+    default: rmsnorm_row_kernel<A, CPT, -1><<<M, 256, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
   }
 }
 
-void launch_rmsnorm(float* x, const uint16_t* gain, float eps, int M, int d, uint16_t* h,
-                    const float* part, int n_part, int part_row0, hipStream_t st) {
+template <class A>
+void rmsnorm_impl(float* x, const uint16_t* gain, float eps, int M, int d, uint16_t* h,
+                  const float* part, int n_part, int part_row0, hipStream_t st) {
   const dim3 grid((M + 3) / 4), block(256);
   if (!part) n_part = 0;
   if (d == 2048 || d == 4096) {  // measured faster at 544 and 8704 rows
-    if (d == 2048) launch_row_norm<1>(x, gain, eps, M, d, h, part, n_part, part_row0, st);
-    else launch_row_norm<2>(x, gain, eps, M, d, h, part, n_part, part_row0, st);
+    if (d == 2048) launch_row_norm<A, 1>(x, gain, eps, M, d, h, part, n_part, part_row0, st);
+    else launch_row_norm<A, 2>(x, gain, eps, M, d, h, part, n_part, part_row0, st);
     return;
   }
-  if (d <= 512) rmsnorm_kernel<1><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
-  else if (d <= 1024) rmsnorm_kernel<2><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
-  else if (d <= 2048) rmsnorm_kernel<4><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
-  else rmsnorm_kernel<8><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
+  if (d <= 512) rmsnorm_kernel<A, 1><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
+  else if (d <= 1024) rmsnorm_kernel<A, 2><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
+  else if (d <= 2048) rmsnorm_kernel<A, 4><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
+  else rmsnorm_kernel<A, 8><<<grid, block, 0, st>>>(x, gain, eps, M, d, h, part, n_part, part_row0);
+}
+
+void launch_rmsnorm(float* x, const uint16_t* gain, float eps, int M, int d, uint16_t* h,
+                    const float* part, int n_part, int part_row0, hipStream_t st, bool f16) {
+  if (f16) rmsnorm_impl<ActF16>(x, gain, eps, M, d, h, part, n_part, part_row0, st);
+  else rmsnorm_impl<ActBf16>(x, gain, eps, M, d, h, part, n_part, part_row0, st);
 }
 
 void launch_residual_reduce(float* x, const float* part, int n_part, int part_row0, int M, int d,
@@ -378,6 +418,17 @@ void launch_residual_reduce(float* x, const float* part, int n_part, int part_ro
   else residual_reduce_kernel<8><<<grid, block, 0, st>>>(x, part, n_part, part_row0, M, d);
 }
 
+template <class A>
+void select_norm_impl(const StepGeom& g, int mode, const int32_t* tokens, const float* x,
+                      const uint16_t* gain, float eps, int d, uint16_t* hf, uint16_t* hf_lo,
+                      int32_t* target, hipStream_t st, int r0, int n, const int32_t* tgt_in, int cp) {
+  dim3 grid((n + 3) / 4), block(256);
+  if (d <= 512) select_norm_kernel<A, 1><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in, cp);
+  else if (d <= 1024) select_norm_kernel<A, 2><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in, cp);
+  else if (d <= 2048) select_norm_kernel<A, 4><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in, cp);
+  else select_norm_kernel<A, 8><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in, cp);
+}
+
 void launch_select_norm(const StepGeom& g, int mode, const int32_t* tokens, const float* x,
                         const uint16_t* gain, float eps, int d, uint16_t* hf, uint16_t* hf_lo,
                         int32_t* target, hipStream_t st, int r0, int n, const int32_t* tgt_in,
@@ -385,12 +436,9 @@ void launch_select_norm(const StepGeom& g, int mode, const int32_t* tokens, cons
   if (mode != 2) { r0 = 0; n = g.B * (mode == 0 ? g.Lb : 2 * g.Lb); }
   if (mode != 0) compact = false;
   if (n <= 0) return;
-  dim3 grid((n + 3) / 4), block(256);
   const int cp = compact ? 1 : 0;
-  if (d <= 512) select_norm_kernel<1><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in, cp);
-  else if (d <= 1024) select_norm_kernel<2><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in, cp);
-  else if (d <= 2048) select_norm_kernel<4><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in, cp);
-  else select_norm_kernel<8><<<grid, block, 0, st>>>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, r0, n, tgt_in, cp);
+  if (g.f16) select_norm_impl<ActF16>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, st, r0, n, tgt_in, cp);
+  else select_norm_impl<ActBf16>(g, mode, tokens, x, gain, eps, d, hf, hf_lo, target, st, r0, n, tgt_in, cp);
 }
 
 void launch_gather_block_rows(const StepGeom& g, const float* x, int d, float* xc, hipStream_t st) {

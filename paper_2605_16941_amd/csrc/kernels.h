@@ -17,6 +17,9 @@ struct StepGeom {
   int S, T, Tp;         // T = S + Ls, Tp = T rounded up to 64
   int mask_id;
   const int32_t* block_start;  // [B] generation-relative start of Y_cur
+  // activation type of the matrix-core operands: 0 bf16, 1 fp16 (the GEMM
+  // weights are then fp16 copies)
+  int f16;
 };
 
 // Absolute index of y_cur,1 for sequence b; finished sequences are clamped to
@@ -33,7 +36,9 @@ __device__ __forceinline__ int row_pos(const StepGeom& g, int b, int t) {
 }
 
 // --------------------------------------------------------------- elementwise
-// x[m] = E[token of row m] (fp32); h[m] = rmsnorm(x[m]) * gain (bf16).
+// Activations h, q, k, v^T, the attention output and u are 16-bit values of
+// the activation type (g.f16 or the f16 argument): bf16 or fp16.
+// x[m] = E[token of row m] (fp32); h[m] = rmsnorm(x[m]) * gain.
 void launch_embed_norm(const StepGeom& g, const int32_t* tokens, const uint16_t* emb, int vocab,
                        const uint16_t* gain, float eps, int d, float* x, uint16_t* h,
                        hipStream_t st);
@@ -42,7 +47,9 @@ void launch_embed_norm(const StepGeom& g, const int32_t* tokens, const uint16_t*
 // [n_part, M - part_row0, d]), are first added to x[m] in order s = 0, 1, ...
 // and x is written back.
 void launch_rmsnorm(float* x, const uint16_t* gain, float eps, int M, int d, uint16_t* h,
-                    const float* part, int n_part, int part_row0, hipStream_t st);
+                    const float* part, int n_part, int part_row0, hipStream_t st, bool f16);
+// out = fp16(in) for n bf16 values (n a multiple of 8), round to nearest even.
+void launch_bf16_to_f16(const uint16_t* in, uint16_t* out, size_t n, hipStream_t st);
 // x[m] += sum_s part[s][m - part_row0] (same order as above), for
 // part_row0 <= m < M.
 void launch_residual_reduce(float* x, const float* part, int n_part, int part_row0, int M, int d,
@@ -55,7 +62,7 @@ void launch_gather_block_rows(const StepGeom& g, const float* x, int d, float* x
 // (-1 for masked).  mode 1: all 2*Lb rows (current then shadow) per sequence.
 // mode 2: response rows r0 .. r0+n-1 of the flattened [B, G] response (row
 // P + j of sequence b for r = b*G + j), target = tgt_in[r].
-// The normed row is written as hi = bf16(y) and lo = bf16(y - hi).
+// The normed row is written as hi = act(y) and lo = act(y - hi).
 // With compact (mode 0 only) x holds the gathered block rows of
 // launch_gather_block_rows instead of the full [B, T] stream.
 void launch_select_norm(const StepGeom& g, int mode, const int32_t* tokens, const float* x,
@@ -64,8 +71,9 @@ void launch_select_norm(const StepGeom& g, int mode, const int32_t* tokens, cons
                         const int32_t* tgt_in = nullptr, bool compact = false);
 
 // --------------------------------------------------------------- GEMM
-// C = A * W^T with A bf16 [M, K] (row stride lda), W bf16 [N, K] (row stride
-// ldw), fp32 accumulation, and one of the fused epilogues below.
+// C = A * W^T with A [M, K] (row stride lda) and W [N, K] (row stride ldw)
+// both bf16, or both fp16 (f16), fp32 accumulation, and one of the fused
+// epilogues below.
 struct RopeOut {      // QKV projection + rotate-half RoPE, head-major outputs
   uint16_t* q;        // [B, H, Tp, hd]
   uint16_t* k;        // [B, H, Tp, hd]
@@ -91,13 +99,14 @@ struct LmStatsOut {   // LM head + streaming softmax statistics per (row, N-tile
 
 enum GemmEpi {
   EPI_QKV_ROPE = 0, EPI_RESIDUAL = 1, EPI_SWIGLU = 2, EPI_LMSTATS = 3,
-  EPI_STORE_F32 = 4,  // out = A W^T (plain bf16 A)
+  EPI_STORE_F32 = 4,  // out = A W^T (plain A)
   EPI_LOGITS = 5      // out = (A + A2) W^T + bias (LM-head precision, test entry point)
 };
 constexpr int kMaxResidualSplits = 8;
 
 struct GemmCall {
   int tile;  // 1 + tile shape index; 0 (zero-initialised call): chosen per call
+  int f16;   // operand type: 0 bf16, 1 fp16 (activation outputs in the same type)
   // Residual epilogue only: rows [0, split_row0) are computed over the whole
   // K and added to outf; with splits > 1 each tile of rows [split_row0, M) is
   // computed as `splits` K-slices (slice s covers columns [s*K/splits,
@@ -106,7 +115,7 @@ struct GemmCall {
   int splits, split_row0;
   float* part;
   const uint16_t* A; int lda;
-  // LM-head epilogues take A as an unevaluated sum A + A2 of two bf16 parts
+  // LM-head epilogues take A as an unevaluated sum A + A2 of two 16-bit parts
   // (hi and lo of an fp32 row): both are multiplied with the same W tile.
   const uint16_t* A2;
   const uint16_t* W; int ldw;
@@ -114,7 +123,7 @@ struct GemmCall {
   GemmEpi epi;
   // residual: x[m*ldc + n] += acc ; store: out[m*ldc + n] = acc (+ bias[n])
   float* outf; int ldc; const float* bias;
-  // swiglu: out[m*ldc + f] = silu(gate) * up (bf16); W rows: gate [0,F), up [F,2F)
+  // swiglu: out[m*ldc + f] = silu(gate) * up (activation type); W rows: gate [0,F), up [F,2F)
   uint16_t* outh; int F;
   RopeOut rope;
   StepGeom geom;
@@ -136,7 +145,7 @@ void plan_residual_gemm(GemmCall& c, size_t part_elems);
 // --------------------------------------------------------------- attention
 // Bidirectional attention with the WINO shadow mask (Sec. 4.2.2): query row
 // t < S sees keys [0, S); shadow query S+j sees keys [0, T) except c0+j.
-// o: bf16 [B*T, H*hd] row-major.
+// q, k, v^T and o in the activation type of g.f16; o: [B*T, H*hd] row-major.
 // compact: query only each sequence's Lb current-block rows and Ls shadow
 // rows; o then holds those rows, [B * (Lb + Ls), H*hd] (current rows first).
 hipError_t launch_attention(const StepGeom& g, const uint16_t* q, const uint16_t* k,

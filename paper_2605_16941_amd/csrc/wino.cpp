@@ -95,6 +95,8 @@ struct wino_ctx {
   const uint16_t* final_norm = nullptr;
   const uint16_t* lm_head = nullptr;
   const float* lm_bias = nullptr;
+  int f16 = 0;                  // activations and GEMM weights in fp16
+  uint16_t* wcopy = nullptr;    // fp16 copies of the GEMM and LM-head weights (f16)
   Layout L{};
   char* ws = nullptr;
   int32_t* h_pinned = nullptr;  // 2 * max_batch ints
@@ -168,7 +170,8 @@ bool shape_supported(const wino_model_config& c) {
   return c.n_layers >= 1 && c.d_model > 0 && c.n_heads > 0 && (c.head_dim == 64 || c.head_dim == 128) &&
          c.d_model == c.n_heads * c.head_dim && c.d_model % 64 == 0 && c.d_model <= 4096 &&
          c.d_ff % 64 == 0 && c.d_ff > 0 && c.vocab % 256 == 0 && c.vocab > 0 &&
-         std::isfinite(c.rope_theta) && c.rope_theta > 0 && std::isfinite(c.rms_eps) && c.rms_eps > 0;
+         std::isfinite(c.rope_theta) && c.rope_theta > 0 && std::isfinite(c.rms_eps) && c.rms_eps > 0 &&
+         (c.act_precision == WINO_ACT_BF16 || c.act_precision == WINO_ACT_FP16);
 }
 
 wino_status validate_params(wino_ctx* ctx, const wino_params* p) {
@@ -186,8 +189,10 @@ wino_status validate_params(wino_ctx* ctx, const wino_params* p) {
   return WINO_OK;
 }
 
-StepGeom make_geom(const wino_params* p, const int32_t* block_start, bool shadow = true) {
+StepGeom make_geom(const wino_ctx* c, const wino_params* p, const int32_t* block_start,
+                   bool shadow = true) {
   StepGeom g{};
+  g.f16 = c->f16;
   g.B = p->batch; g.P = p->prompt_len; g.G = p->gen_len; g.Lb = p->block_len;
   g.Ls = shadow ? g.Lb : 0;
   g.S = g.P + g.G; g.T = g.S + g.Ls; g.Tp = round64(g.T);
@@ -244,6 +249,7 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
   }
   for (int l = 0; l < m.n_layers && 2 * l < n_sub; ++l) {
     GemmCall qc{};
+    qc.f16 = c->f16;
     qc.A = c->h(); qc.lda = d; qc.W = c->w_qkv[l]; qc.ldw = d;
     qc.M = M; qc.N = 3 * d; qc.K = d; qc.epi = EPI_QKV_ROPE;
     qc.rope = RopeOut{c->q(), c->k(), c->vt(), c->rope_tab(), H, hd};
@@ -271,6 +277,7 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
       br.done(0, 8.0 * Mr * d);
     }
     GemmCall oc{};
+    oc.f16 = c->f16;
     oc.A = c->att(); oc.lda = d; oc.W = c->w_o[l]; oc.ldw = d;
     oc.M = Mr; oc.N = d; oc.K = d; oc.epi = EPI_RESIDUAL; oc.outf = xr; oc.ldc = d;
     {
@@ -283,12 +290,14 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
     if (2 * l + 1 >= n_sub) break;
     {
       Bracket br(c, K_RMSNORM, st);
-      launch_rmsnorm(xr, c->ffn_norm[l], m.rms_eps, Mr, d, c->h(), c->part(), pend.n, pend.row0, st);
+      launch_rmsnorm(xr, c->ffn_norm[l], m.rms_eps, Mr, d, c->h(), c->part(), pend.n, pend.row0, st,
+                     c->f16);
       HIP_TRY(c, hipGetLastError());
       br.done(0, norm_bytes(Mr, d, pend));
       pend = Pending{};
     }
     GemmCall gc{};
+    gc.f16 = c->f16;
     gc.A = c->h(); gc.lda = d; gc.W = c->w_gu[l]; gc.ldw = d;
     gc.M = Mr; gc.N = 2 * F; gc.K = d; gc.epi = EPI_SWIGLU; gc.outh = c->u(); gc.ldc = F; gc.F = F;
     {
@@ -297,6 +306,7 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
       br.done(2.0 * Mr * 2.0 * F * d, 2.0 * ((double)Mr * d + 2.0 * F * d + (double)Mr * F));
     }
     GemmCall dc{};
+    dc.f16 = c->f16;
     dc.A = c->u(); dc.lda = F; dc.W = c->w_down[l]; dc.ldw = F;
     dc.M = Mr; dc.N = d; dc.K = F; dc.epi = EPI_RESIDUAL; dc.outf = xr; dc.ldc = d;
     {
@@ -309,7 +319,7 @@ wino_status run_forward(wino_ctx* c, const StepGeom& g, const int32_t* tokens, i
     if (l + 1 < m.n_layers && 2 * (l + 1) < n_sub) {
       Bracket br(c, K_RMSNORM, st);
       launch_rmsnorm(c->x(), c->attn_norm[l + 1], m.rms_eps, M, d, c->h(), c->part(), pend.n,
-                     pend.row0, st);
+                     pend.row0, st, c->f16);
       HIP_TRY(c, hipGetLastError());
       br.done(0, norm_bytes(M, d, pend));
       pend = Pending{};
@@ -335,7 +345,7 @@ wino_status step_impl(wino_ctx* c, const wino_params* p, int32_t* tokens, int32_
                       int32_t* final_step = nullptr) {
   const wino_model_config& m = c->cfg;
   shadow = shadow && p->tokens_per_step == 0;  // the baselines never verify
-  const StepGeom g = make_geom(p, block_start, shadow);
+  const StepGeom g = make_geom(c, p, block_start, shadow);
   wino_status s = run_forward(c, g, tokens, 2 * m.n_layers, st, true);
   if (s != WINO_OK) return s;
   const int R = g.B * g.Lb;
@@ -347,6 +357,7 @@ wino_status step_impl(wino_ctx* c, const wino_params* p, int32_t* tokens, int32_
     br.done(0, (double)R * m.d_model * 6);
   }
   GemmCall lc{};
+  lc.f16 = c->f16;
   lc.A = c->hf(); lc.A2 = c->hf_lo(); lc.lda = m.d_model; lc.W = c->lm_head; lc.ldw = m.d_model;
   lc.M = R; lc.N = m.vocab; lc.K = m.d_model; lc.epi = EPI_LMSTATS;
   const int bn = gemm_tile_n(lc);
@@ -544,6 +555,36 @@ wino_status wino_create(const wino_model_config* cfg, const wino_weights* w, int
     wino_destroy(c);
     return WINO_ERR_HIP;
   }
+  if (cfg->act_precision == WINO_ACT_FP16) {
+    // fp16 copies of every matrix the matrix cores multiply (bf16 -> fp16 is
+    // exact for |w| >= 2^-17 and moves smaller values by at most 2^-25)
+    const size_t d = cfg->d_model, F = cfg->d_ff;
+    const size_t per_layer = 3 * d * d + d * d + 2 * F * d + d * F;
+    const size_t total = per_layer * cfg->n_layers + (size_t)cfg->vocab * d;
+    if (hipMalloc(&c->wcopy, total * 2) != hipSuccess) {
+      c->wcopy = nullptr;
+      wino_destroy(c);
+      return WINO_ERR_NO_MEMORY;
+    }
+    c->f16 = 1;
+    uint16_t* dst = c->wcopy;
+    auto convert = [&](const uint16_t*& w, size_t n) {
+      launch_bf16_to_f16(w, dst, n, nullptr);
+      w = dst;
+      dst += n;
+    };
+    for (int l = 0; l < cfg->n_layers; ++l) {
+      convert(c->w_qkv[l], 3 * d * d);
+      convert(c->w_o[l], d * d);
+      convert(c->w_gu[l], 2 * F * d);
+      convert(c->w_down[l], d * F);
+    }
+    convert(c->lm_head, (size_t)cfg->vocab * d);
+    if (hipGetLastError() != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+      wino_destroy(c);
+      return WINO_ERR_HIP;
+    }
+  }
   *out = c;
   return WINO_OK;
 }
@@ -553,6 +594,7 @@ wino_status wino_destroy(wino_ctx* c) {
   drain_profile(c);
   for (hipEvent_t e : c->pool) hipEventDestroy(e);
   if (c->ws) hipFree(c->ws);
+  if (c->wcopy) hipFree(c->wcopy);
   if (c->h_pinned) hipHostFree(c->h_pinned);
   delete c;
   return WINO_OK;
@@ -602,7 +644,7 @@ wino_status wino_decode_block(wino_ctx* c, const wino_params* p, int32_t* d_toke
   const int cap = block_cap(p);
   HIP_TRY(c, hipMemsetAsync(c->block_steps(), 0, sizeof(int32_t) * 2 * c->max_batch, st));
   int32_t* h_nv = c->h_pinned + 2 * B;  // next_verify per sequence
-  HIP_TRY(c, launch_probe_verify(make_geom(p, d_block_start), d_tokens, c->next_verify(), st));
+  HIP_TRY(c, launch_probe_verify(make_geom(c, p, d_block_start), d_tokens, c->next_verify(), st));
   HIP_TRY(c, hipMemcpyAsync(h_nv, c->next_verify(), sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
   HIP_TRY(c, hipStreamSynchronize(st));
   for (int it = 0;; ++it) {
@@ -643,7 +685,7 @@ wino_status wino_decode(wino_ctx* c, const wino_params* p, int32_t* d_tokens, in
   int forwards = 0;
   int32_t* h_nv = c->h_pinned + 2 * B;  // next_verify per sequence
   // blocks holding no mask at the start (a resumed or pre-filled state) are skipped
-  HIP_TRY(c, launch_probe_verify(make_geom(p, d_block_start), d_tokens, c->next_verify(), st,
+  HIP_TRY(c, launch_probe_verify(make_geom(c, p, d_block_start), d_tokens, c->next_verify(), st,
                                  d_block_start, bsteps));
   HIP_TRY(c, hipMemcpyAsync(h_nv, c->next_verify(), sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
   HIP_TRY(c, hipMemcpyAsync(c->h_pinned, d_block_start, sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
@@ -688,10 +730,11 @@ wino_status wino_row_losses(wino_ctx* c, const wino_params* p, const int32_t* d_
   const wino_model_config& m = c->cfg;
   // a plain forward: no shadow rows, so the block cursor is never read for
   // positions (any valid [B] int32 buffer serves as its pointer)
-  const StepGeom g = make_geom(p, c->block_steps(), false);
+  const StepGeom g = make_geom(c, p, c->block_steps(), false);
   s = run_forward(c, g, d_tokens, 2 * m.n_layers, st);
   if (s != WINO_OK) return s;
   GemmCall lc{};
+  lc.f16 = c->f16;
   lc.A = c->hf(); lc.A2 = c->hf_lo(); lc.lda = m.d_model; lc.W = c->lm_head; lc.ldw = m.d_model;
   lc.N = m.vocab; lc.K = m.d_model; lc.epi = EPI_LMSTATS;
   const long total = (long)g.B * g.G;
@@ -764,13 +807,14 @@ wino_status wino_debug_logits(wino_ctx* c, const wino_params* p, const int32_t* 
   if (!d_tokens || !d_block_start || !d_logits) return WINO_ERR_INVALID_ARG;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const wino_model_config& m = c->cfg;
-  const StepGeom g = make_geom(p, d_block_start);
+  const StepGeom g = make_geom(c, p, d_block_start);
   s = run_forward(c, g, d_tokens, 2 * m.n_layers, st);
   if (s != WINO_OK) return s;
   launch_select_norm(g, 1, d_tokens, c->x(), c->final_norm, m.rms_eps, m.d_model, c->hf(), c->hf_lo(),
                      c->target(), st);
   HIP_TRY(c, hipGetLastError());
   GemmCall lc{};
+  lc.f16 = c->f16;
   lc.A = c->hf(); lc.A2 = c->hf_lo(); lc.lda = m.d_model; lc.W = c->lm_head; lc.ldw = m.d_model;
   lc.M = g.B * 2 * g.Lb; lc.N = m.vocab; lc.K = m.d_model; lc.epi = EPI_LOGITS;
   lc.outf = d_logits; lc.ldc = m.vocab; lc.bias = c->lm_bias;
@@ -789,7 +833,7 @@ wino_status wino_debug_forward(wino_ctx* c, const wino_params* p, const int32_t*
   if (!d_tokens || !d_block_start || !d_out) return WINO_ERR_INVALID_ARG;
   if (n_sublayers < 0 || n_sublayers > 2 * c->cfg.n_layers) return WINO_ERR_INVALID_ARG;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const StepGeom g = make_geom(p, d_block_start);
+  const StepGeom g = make_geom(c, p, d_block_start);
   s = run_forward(c, g, d_tokens, n_sublayers, st);
   if (s != WINO_OK) return s;
   HIP_TRY(c, hipMemcpyAsync(d_out, c->x(), sizeof(float) * (size_t)g.B * g.T * c->cfg.d_model,

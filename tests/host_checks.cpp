@@ -58,6 +58,8 @@ int main() {
   CHECK(wino_create(&bad, &w, 1, 112, &ctx) == WINO_ERR_UNSUPPORTED);
   bad = cfg; bad.rms_eps = NAN;
   CHECK(wino_create(&bad, &w, 1, 112, &ctx) == WINO_ERR_UNSUPPORTED);
+  bad = cfg; bad.act_precision = 2;
+  CHECK(wino_create(&bad, &w, 1, 112, &ctx) == WINO_ERR_UNSUPPORTED);
   CHECK(wino_create(&cfg, &w, 1, 112, &ctx) == WINO_ERR_INVALID_ARG);  // null weights
   CHECK(ctx == nullptr);
 

@@ -35,7 +35,7 @@ def test_every_declared_symbol_is_exported(abi):
 
 
 def test_struct_sizes_match_header_layout(abi):
-    assert C.sizeof(abi.wino_model_config) == 32
+    assert C.sizeof(abi.wino_model_config) == 36
     assert C.sizeof(abi.wino_params) == 40
     assert C.sizeof(abi.wino_row_stats) == 24
     assert C.sizeof(abi.wino_row_loss) == 16

@@ -38,13 +38,14 @@ def P():
     return pkg
 
 
-def teacher_forced(P, variant, tau1, tau2, lb=16, B=2, seed=1, tok_seed=5, delta_margin=False):
+def teacher_forced(P, variant, tau1, tau2, lb=16, B=2, seed=1, tok_seed=5, delta_margin=False, act=0):
     """Every step of the float64 oracle's decode of B sequences, each fed to
     one GPU step (the oracle's state in, the GPU's decisions compared).
-    Returns the compared counts per decision kind and oracle-side counts."""
+    Returns the compared counts per decision kind and oracle-side counts.
+    act: the library's activation type (P.ACT_BF16 or P.ACT_FP16)."""
     cfg, w = tiny(variant, seed=seed)
     from helpers import to_device
-    model = P.WinoModel(cfg, to_device(w), B, P_LEN + G_LEN + lb)
+    model = P.WinoModel(cfg, to_device(w), B, P_LEN + G_LEN + lb, act_precision=act)
     prm_c = P.make_params(B, P_LEN, G_LEN, lb, cfg.mask_id, tau1, tau2)
     prm = oracle_params(prm_c)
     tok0 = batch_tokens(cfg, B, P_LEN, G_LEN, seed=tok_seed)
@@ -139,6 +140,20 @@ def test_mask_id_holding_the_row_max_teacher_forced(P):
           f"delta up to {worst_delta:.2e}, GPU |dp| vs float64 {worst_dp:.2e}")
     assert n >= 64 and got["draft"] >= 5 and got["remask"] >= 5
     assert worst_dp <= 3 * worst_delta + 1e-4
+
+
+@pytest.mark.parametrize("variant,tau1,tau2", [("midmask", 0.7, 0.9), ("wide", 0.7, 0.9), ("wide", 0.5, 0.9),
+                                               ("literal", 0.7, 0.9)])
+def test_contract_fp16_activations(P, variant, tau1, tau2):
+    """With fp16 activations the GPU's probabilities stay within 1e-3 of
+    float64 on these workloads - including the one whose confidences cluster
+    at tau1 - so the contract holds at margin 1e-3 on all of them."""
+    got, seen, worst_dp, _, block_steps = teacher_forced(P, variant, tau1, tau2, act=P.ACT_FP16)
+    n = sum(v for k, v in got.items() if k != "verify_keep")
+    print(f"fp16 {variant} tau {tau1}/{tau2}: compared {n} decisions {got}; oracle steps per block "
+          f"{block_steps}; GPU |dp| vs float64 {worst_dp:.2e}")
+    assert n >= 64
+    assert worst_dp < MARGIN
 
 
 def sharp_margin(prov16, prm, mask_id):
