@@ -391,12 +391,14 @@ def full_shape_state(cfg, B, p, g, lb, image):
     return tok0, bstart
 
 
-def full_shape_check(P, cfg, wd, B, p, g, lb, tau1, tok0, bstart, check, wide):
+def full_shape_check(P, cfg, wd, B, p, g, lb, tau1, tok0, bstart, check, wide, act=0):
     """One GPU step at a full shape, checked for the sequences in `check`
     against the float64 oracle: logits within 2e-2, decisions at margin 1e-3
-    (literal init: the contract) or max(1e-3, 3*delta) (wide init, labelled)."""
+    (literal init: the contract) or max(1e-3, 3*delta) (wide init, labelled).
+    With fp16 activations (act) the GPU's probabilities must also lie within
+    1e-3 of float64."""
     from helpers import LOGIT_TOL, rowwise_rel_err
-    model = P.WinoModel(cfg, wd, B, p + g + lb)
+    model = P.WinoModel(cfg, wd, B, p + g + lb, act_precision=act)
     prm_c = P.make_params(B, p, g, lb, cfg.mask_id, tau1, 0.9)
     prm = oracle_params(prm_c)
     gt, gf, gnm, gst, gstats = gpu_step(P, model, prm_c, tok0, bstart, [1] * B)
@@ -430,15 +432,18 @@ def full_shape_check(P, cfg, wd, B, p, g, lb, tau1, tok0, bstart, check, wide):
               f"{n}/{lb} decisions compared at margin {margin:.1e} {c}" + (f"; delta {delta:.2e}" if wide else ""))
         if wide:
             assert dp64 <= 3 * delta + 1e-4
+        if act == P.ACT_FP16:
+            assert dp64 < MARGIN
     assert total >= len(check) * lb // 2
     return w
 
 
 @pytest.mark.slow
-def test_contract_full_model_step_bs1(P):
+@pytest.mark.parametrize("act", ["bf16", "fp16"])
+def test_contract_full_model_step_bs1(P, act):
     """All 32 layers at the LLaDA-8B shape, batch 1, literal init (the
     benchmark's bs1 configuration): the contract at margin 1e-3 against the
-    float64 oracle of the whole step."""
+    float64 oracle of the whole step, with bf16 and with fp16 activations."""
     cfg, wd = big_weights("llada8b", gain_std=0.0)
     B, p, g, lb = 1, 256, 256, 32
     pr = wi.prompts(cfg, B, p, seed=1000).numpy()
@@ -447,7 +452,8 @@ def test_contract_full_model_step_bs1(P):
     tok0[0, p:p + lb] = rng.integers(0, cfg.mask_id, lb)
     sel = np.arange(p + lb, p + 2 * lb)[rng.random(lb) < 0.5]
     tok0[0, sel] = rng.integers(0, cfg.mask_id, len(sel))
-    full_shape_check(P, cfg, wd, B, p, g, lb, 0.7, tok0, [lb], [0], wide=False)
+    full_shape_check(P, cfg, wd, B, p, g, lb, 0.7, tok0, [lb], [0], wide=False,
+                     act=P.ACT_FP16 if act == "fp16" else P.ACT_BF16)
 
 
 @pytest.mark.slow
