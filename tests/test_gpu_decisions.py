@@ -239,6 +239,27 @@ def test_iterating_decode_teacher_forced(P, tau1, tau2):
     model.close()
 
 
+def test_decode_teacher_forced_fp16_activations(P):
+    """The workload whose confidences cluster at tau1 ('midmask') through
+    wino_decode with fp16 activations, one forward per call with the
+    oracle's state fed in before each: every position the float64 oracle
+    fixes at margin 1e-3 comes out as the oracle's (the decode loop's shadow
+    choice, block advance and step cap included)."""
+    cfg, w = tiny("midmask", seed=1)
+    from helpers import to_device
+    B, lb = 2, 16
+    model = P.WinoModel(cfg, to_device(w), B, P_LEN + G_LEN + lb, act_precision=P.ACT_FP16)
+    prm_c = P.make_params(B, P_LEN, G_LEN, lb, cfg.mask_id, 0.7, 0.9)
+    prm = oracle_params(prm_c)
+    tok0 = batch_tokens(cfg, B, P_LEN, G_LEN, seed=5)
+    compared, _, forwards, trajs = decode_prefix_compare(P, model, prm_c, prm, fp64_provider(w, cfg), tok0,
+                                                         "midmask fp16", teacher_forced=True)
+    print(f"midmask fp16: positions compared {compared} over {[len(t) for t in trajs]} steps")
+    assert forwards == max(len(t) for t in trajs)
+    assert sum(compared) >= 200
+    model.close()
+
+
 def test_resume_splits_match_uninterrupted(P):
     """Checkpoint / resume: the decode state is (tokens, block_start,
     block_steps).  A decode stopped after k forwards (mid-block and at block
