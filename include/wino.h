@@ -140,11 +140,13 @@ typedef struct {
 /* Create a context for `cfg` with the given weights.  The context owns a
  * device workspace sized for up to max_batch sequences of up to max_seq =
  * prompt_len + gen_len + block_len extended rows (the current device at the
- * time of the call).  Returns WINO_ERR_NO_MEMORY if it cannot be allocated. */
+ * time of the call), and with WINO_ACT_FP16 the fp16 copies of the weight
+ * matrices.  Returns WINO_ERR_NO_MEMORY if they cannot be allocated. */
 wino_status wino_create(const wino_model_config* cfg, const wino_weights* w,
                         int32_t max_batch, int32_t max_seq, wino_ctx** out);
 wino_status wino_destroy(wino_ctx* ctx);
-/* Workspace bytes wino_create would allocate. */
+/* Workspace bytes wino_create would allocate (without the fp16 weight copies
+ * of WINO_ACT_FP16: 2 bytes per parameter of the weight matrices). */
 size_t wino_workspace_bytes(const wino_model_config* cfg, int32_t max_batch, int32_t max_seq);
 
 /* One WINO step (Eq. 4) for every sequence of the batch.
