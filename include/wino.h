@@ -68,8 +68,9 @@ typedef struct wino_ctx wino_ctx;
  * confidences sit near a threshold), at the cost of fp16 copies of every
  * weight matrix (2 bytes per parameter of the QKV, O, gate/up, down and LM
  * head matrices, allocated by wino_create beside the workspace) and of fp16
- * matrix-core throughput; activations must stay within fp16's range
- * (|x| < 65504).  Zero-initialised configurations get WINO_ACT_BF16. */
+ * matrix-core throughput; weights and activations must stay within fp16's
+ * range (|x| < 65504; weights of magnitude below 2^-17 move by at most
+ * 2^-25 in the copy).  Zero-initialised configurations get WINO_ACT_BF16. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, head_dim, d_ff, vocab;
   float rope_theta; /* rotate-half RoPE base                         */
@@ -141,7 +142,9 @@ typedef struct {
  * device workspace sized for up to max_batch sequences of up to max_seq =
  * prompt_len + gen_len + block_len extended rows (the current device at the
  * time of the call), and with WINO_ACT_FP16 the fp16 copies of the weight
- * matrices.  Returns WINO_ERR_NO_MEMORY if they cannot be allocated. */
+ * matrices.  Returns WINO_ERR_NO_MEMORY if they cannot be allocated, and
+ * with WINO_ACT_FP16 WINO_ERR_UNSUPPORTED if a weight matrix holds a value
+ * with no finite fp16 copy (|w| > 65504, or not finite). */
 wino_status wino_create(const wino_model_config* cfg, const wino_weights* w,
                         int32_t max_batch, int32_t max_seq, wino_ctx** out);
 wino_status wino_destroy(wino_ctx* ctx);

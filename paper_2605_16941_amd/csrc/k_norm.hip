@@ -331,26 +331,32 @@ __global__ __launch_bounds__(256) void gather_block_rows_kernel(StepGeom g, cons
 // Weights bf16 -> fp16 (round to nearest even), 8 elements per thread; n is
 // a multiple of 8.
 __global__ __launch_bounds__(256) void bf16_to_f16_kernel(const uint16_t* __restrict__ in,
-                                                          uint16_t* __restrict__ out, size_t n8) {
+                                                          uint16_t* __restrict__ out, size_t n8,
+                                                          int* __restrict__ overflow) {
+  bool bad = false;
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n8; i += (size_t)gridDim.x * 256) {
     const uint4 raw = reinterpret_cast<const uint4*>(in)[i];
     const uint32_t* w = &raw.x;
     uint4 o;
     uint32_t* op = &o.x;
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
+    for (int e = 0; e < 4; ++e) {
       op[e] = ActF16::pack2(__uint_as_float(w[e] << 16), __uint_as_float(w[e] & 0xFFFF0000u));
+      // an all-ones exponent: the value overflowed fp16 (or was not finite)
+      bad |= (op[e] & 0x7C00u) == 0x7C00u || (op[e] & 0x7C000000u) == 0x7C000000u;
+    }
     reinterpret_cast<uint4*>(out)[i] = o;
   }
+  if (bad) *overflow = 1;
 }
 
 }  // namespace
 
-void launch_bf16_to_f16(const uint16_t* in, uint16_t* out, size_t n, hipStream_t st) {
+void launch_bf16_to_f16(const uint16_t* in, uint16_t* out, size_t n, int* overflow, hipStream_t st) {
   const size_t n8 = n / 8;
   if (n8 == 0) return;
   const size_t blocks = std::min<size_t>((n8 + 255) / 256, 8192);
-  bf16_to_f16_kernel<<<blocks, 256, 0, st>>>(in, out, n8);
+  bf16_to_f16_kernel<<<blocks, 256, 0, st>>>(in, out, n8, overflow);
 }
 
 // The library accepts d <= 4096 (up to 8 chunks of 8 elements per lane).

@@ -48,8 +48,10 @@ void launch_embed_norm(const StepGeom& g, const int32_t* tokens, const uint16_t*
 // and x is written back.
 void launch_rmsnorm(float* x, const uint16_t* gain, float eps, int M, int d, uint16_t* h,
                     const float* part, int n_part, int part_row0, hipStream_t st, bool f16);
-// out = fp16(in) for n bf16 values (n a multiple of 8), round to nearest even.
-void launch_bf16_to_f16(const uint16_t* in, uint16_t* out, size_t n, hipStream_t st);
+// out = fp16(in) for n bf16 values (n a multiple of 8), round to nearest even;
+// *overflow is set to 1 if an output is not finite (|in| beyond fp16's range,
+// or a non-finite input), else left as it is.
+void launch_bf16_to_f16(const uint16_t* in, uint16_t* out, size_t n, int* overflow, hipStream_t st);
 // x[m] += sum_s part[s][m - part_row0] (same order as above), for
 // part_row0 <= m < M.
 void launch_residual_reduce(float* x, const float* part, int n_part, int part_row0, int M, int d,

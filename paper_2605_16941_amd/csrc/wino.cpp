@@ -567,9 +567,12 @@ wino_status wino_create(const wino_model_config* cfg, const wino_weights* w, int
       return WINO_ERR_NO_MEMORY;
     }
     c->f16 = 1;
+    // the overflow flag lives in the first word of the (zeroed) workspace
+    // until the copies are checked
+    int* overflow = reinterpret_cast<int*>(c->ws);
     uint16_t* dst = c->wcopy;
     auto convert = [&](const uint16_t*& w, size_t n) {
-      launch_bf16_to_f16(w, dst, n, nullptr);
+      launch_bf16_to_f16(w, dst, n, overflow, nullptr);
       w = dst;
       dst += n;
     };
@@ -580,9 +583,17 @@ wino_status wino_create(const wino_model_config* cfg, const wino_weights* w, int
       convert(c->w_down[l], d * F);
     }
     convert(c->lm_head, (size_t)cfg->vocab * d);
-    if (hipGetLastError() != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+    int h_overflow = 0;
+    if (hipGetLastError() != hipSuccess || hipDeviceSynchronize() != hipSuccess ||
+        hipMemcpy(&h_overflow, overflow, sizeof(int), hipMemcpyDeviceToHost) != hipSuccess ||
+        hipMemset(overflow, 0, sizeof(int)) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
       wino_destroy(c);
       return WINO_ERR_HIP;
+    }
+    // a weight beyond fp16's range has no fp16 copy
+    if (h_overflow) {
+      wino_destroy(c);
+      return WINO_ERR_UNSUPPORTED;
     }
   }
   *out = c;

@@ -112,6 +112,27 @@ def test_ragged_shapes_fp16_activations(P, p, g, lb, B):
     assert errs[P.ACT_FP16] < errs[P.ACT_BF16] and errs[P.ACT_FP16] < 2e-3
 
 
+def test_fp16_copies_reject_weights_beyond_fp16_range(P):
+    """wino_create in fp16 mode refuses weights with no finite fp16 copy (a
+    value beyond 65504 in any multiplied matrix) and accepts the largest bf16
+    value inside that range (65280)."""
+    cfg, w = tiny("literal", seed=2)
+    for key, layer, val, ok in (("w_down", 1, 65280.0, True), ("w_down", 1, 66000.0, False),
+                                ("w_qkv", 0, -1.0e5, False), ("lm_head", None, 7.0e4, False)):
+        wd = to_device(w)
+        tgt = wd["lm_head"] if layer is None else wd["layers"][layer][key]
+        tgt.view(-1)[12345 % tgt.numel()] = val
+        torch.cuda.synchronize()
+        if ok:
+            P.WinoModel(cfg, wd, 1, 64, act_precision=P.ACT_FP16).close()
+            continue
+        with pytest.raises(P.WinoError) as e:
+            P.WinoModel(cfg, wd, 1, 64, act_precision=P.ACT_FP16)
+        assert e.value.status == -6, (key, val)
+        # the same weights are accepted with bf16 activations
+        P.WinoModel(cfg, wd, 1, 64).close()
+
+
 @pytest.mark.parametrize("p,g,lb,B", [(0, 21, 7, 3), (6, 24, 3, 2), (13, 20, 20, 1)])
 def test_ragged_shapes_forward_and_decode(P, p, g, lb, B):
     """Ragged edge cases: no prompt, T = P + G + L_b not a multiple of 8 (the
