@@ -99,7 +99,7 @@ struct wino_ctx {
   uint16_t* wcopy = nullptr;    // fp16 copies of the GEMM and LM-head weights (f16)
   Layout L{};
   char* ws = nullptr;
-  int32_t* h_pinned = nullptr;  // 2 * max_batch ints
+  int32_t* h_pinned = nullptr;  // 4 * max_batch ints (block starts, step counts, next_verify)
   std::string err;
   // profiling
   uint32_t prof_mask = 0;
