@@ -171,9 +171,10 @@ wino_status wino_step(wino_ctx* ctx, const wino_params* p, int32_t* d_tokens,
                       int32_t* d_n_masked, wino_row_stats* d_stats, void* stream);
 
 /* Iterate wino_step on the current block of every sequence until none holds a
- * mask (Sec. 4.2.3).  d_final_step int32 [batch, gen_len] (device, or NULL)
- * is written as in wino_decode.  h_steps [batch] receives the steps each
- * sequence took.  Synchronises `stream` once per step. */
+ * mask (Sec. 4.2.3); if none holds one at the start, no forward runs.
+ * d_final_step int32 [batch, gen_len] (device, or NULL) is written as in
+ * wino_decode.  h_steps [batch] receives the steps each sequence took.
+ * Synchronises `stream` once per step. */
 wino_status wino_decode_block(wino_ctx* ctx, const wino_params* p, int32_t* d_tokens,
                               const int32_t* d_block_start, int32_t* d_final_step,
                               int32_t* h_steps, void* stream);

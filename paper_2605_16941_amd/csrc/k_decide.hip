@@ -306,7 +306,7 @@ __global__ __launch_bounds__(64) void probe_verify_kernel(const StepGeom g,
                                                           const int32_t* __restrict__ tokens,
                                                           int32_t* __restrict__ next_verify,
                                                           int32_t* block_start, int32_t* block_steps,
-                                                          int advance) {
+                                                          int advance, int32_t* n_masked) {
   const int b = blockIdx.x, lane = threadIdx.x;
   int bs = g.block_start[b];
   const int32_t* resp = tokens + (size_t)b * g.S + g.P;
@@ -334,7 +334,10 @@ __global__ __launch_bounds__(64) void probe_verify_kernel(const StepGeom g,
   }
   nmask = (int)wave_sum((float)nmask);
   nkeep = (int)wave_sum((float)nkeep);
-  if (lane == 0) next_verify[b] = nmask > 0 && nkeep > 0;
+  if (lane == 0) {
+    next_verify[b] = nmask > 0 && nkeep > 0;
+    if (n_masked) n_masked[b] = nmask;
+  }
 }
 
 // Partial softmax statistics of one chunk of CHUNK ids of one needed logits
@@ -497,9 +500,10 @@ hipError_t launch_loss_merge(const LmStatsOut& lm, int R, void* out, hipStream_t
 }
 
 hipError_t launch_probe_verify(const StepGeom& g, const int32_t* tokens, int32_t* next_verify,
-                               hipStream_t st, int32_t* block_start, int32_t* block_steps) {
+                               hipStream_t st, int32_t* block_start, int32_t* block_steps,
+                               int32_t* n_masked) {
   probe_verify_kernel<<<g.B, 64, 0, st>>>(g, tokens, next_verify, block_start, block_steps,
-                                          block_start != nullptr);
+                                          block_start != nullptr, n_masked);
   return hipGetLastError();
 }
 

@@ -191,13 +191,14 @@ hipError_t launch_decide(const DecideArgs& a, hipStream_t st);
 // required): out[r] = {entropy, nll of the target, greedy confidence, argmax}
 // (wino_loss_row layout).
 hipError_t launch_loss_merge(const LmStatsOut& lm, int R, void* out, hipStream_t st);
-// next_verify[b] as above for the state before any step (fused-step layout).
-// With block_start (the same array as g.block_start, writable), a sequence
-// whose Y_cur holds no mask first moves to the first later block holding one
-// (or to G) and its block_steps entry (if given) restarts at 0.
+// next_verify[b] as above for the state before any step (fused-step layout),
+// and n_masked[b] (if given) the masks in that Y_cur (0 for a finished
+// sequence).  With block_start (the same array as g.block_start, writable), a
+// sequence whose Y_cur holds no mask first moves to the first later block
+// holding one (or to G) and its block_steps entry (if given) restarts at 0.
 hipError_t launch_probe_verify(const StepGeom& g, const int32_t* tokens, int32_t* next_verify,
                                hipStream_t st, int32_t* block_start = nullptr,
-                               int32_t* block_steps = nullptr);
+                               int32_t* block_steps = nullptr, int32_t* n_masked = nullptr);
 
 // Standalone epilogue statistics: for each (b, l) pick the current row
 // (masked) or the shadow row (unmasked) of bf16 logits [B, 2Lb, V], and write

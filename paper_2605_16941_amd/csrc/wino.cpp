@@ -655,10 +655,15 @@ wino_status wino_decode_block(wino_ctx* c, const wino_params* p, int32_t* d_toke
   const int cap = block_cap(p);
   HIP_TRY(c, hipMemsetAsync(c->block_steps(), 0, sizeof(int32_t) * 2 * c->max_batch, st));
   int32_t* h_nv = c->h_pinned + 2 * B;  // next_verify per sequence
-  HIP_TRY(c, launch_probe_verify(make_geom(c, p, d_block_start), d_tokens, c->next_verify(), st));
+  HIP_TRY(c, launch_probe_verify(make_geom(c, p, d_block_start), d_tokens, c->next_verify(), st,
+                                 nullptr, nullptr, c->n_masked()));
   HIP_TRY(c, hipMemcpyAsync(h_nv, c->next_verify(), sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
+  HIP_TRY(c, hipMemcpyAsync(c->h_pinned, c->n_masked(), sizeof(int32_t) * B, hipMemcpyDeviceToHost, st));
   HIP_TRY(c, hipStreamSynchronize(st));
-  for (int it = 0;; ++it) {
+  // no current block holds a mask: nothing to decode, no forward
+  bool any_mask = false;
+  for (int b = 0; b < B; ++b) any_mask |= c->h_pinned[b] > 0;
+  for (int it = 0; any_mask; ++it) {
     s = step_impl(c, p, d_tokens, const_cast<int32_t*>(d_block_start), c->block_steps(), nullptr,
                   c->n_masked(), nullptr, 0, c->seq_steps(), need_shadow(p, h_nv), st, d_final_step);
     if (s != WINO_OK) return s;

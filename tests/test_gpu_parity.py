@@ -372,6 +372,15 @@ def test_decode_block_matches_oracle(P, mixed):
             assert np.array_equal(fin[b], t[p:]), f"seq {b}: finalization steps differ"
             n_cmp += 1
     assert n_cmp > 0
+    # the same blocks again: none holds a mask, so the call runs no forward
+    P.wino_profile(model.ctx, 1)  # class 0: the embedding, once per forward
+    P.wino_profile_read(model.ctx)
+    tok_done = tok.clone()
+    assert P.wino_decode_block(model.ctx, prm_c, tok, bs) == [0] * B
+    torch.cuda.synchronize()
+    assert P.wino_profile_read(model.ctx)[P.wino_kernel_class_name(0)]["launches"] == 0
+    assert torch.equal(tok, tok_done)
+    P.wino_profile(model.ctx, 0)
     model.close()
 
 
