@@ -23,6 +23,10 @@
  *   and leave outputs untouched.  HIP runtime failures return WINO_ERR_HIP;
  *   the text is available from wino_last_error(ctx).
  * - A context is not thread-safe; calls that overlap on one context race.
+ * - Device pointers must come from the HIP runtime the library is loaded
+ *   against.  A process with two copies of the runtime (the system's and one
+ *   bundled with a framework) must load the framework first, so that the
+ *   library's runtime dependency resolves to the framework's copy.
  *
  * Readings of points the paper leaves open (all documented with the flags):
  * greedy argmax decoding; the draft's max/argmax exclude the mask id (which

@@ -28,6 +28,15 @@ def _load():
         raise ImportError(
             f"libwino.so not found at {_LIB_PATH}; build it with "
             "`python paper_2605_16941_amd/build.py` (hipcc, gfx950)")
+    # The library must run on the HIP runtime that allocates the device memory
+    # it is handed.  torch ships its own copy of that runtime: loaded first,
+    # it satisfies the library's runtime dependency; loaded after the library,
+    # it joins the system copy the library pulled in, and pointers of one copy
+    # are unknown to the other (wino_create then fails with WINO_ERR_HIP).
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     return C.CDLL(_LIB_PATH)
 
 

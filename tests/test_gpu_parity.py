@@ -112,6 +112,26 @@ def test_ragged_shapes_fp16_activations(P, p, g, lb, B):
     assert errs[P.ACT_FP16] < errs[P.ACT_BF16] and errs[P.ACT_FP16] < 2e-3
 
 
+def test_package_imported_before_torch(P):
+    """A process that imports the package before torch still runs the library
+    on torch's HIP runtime: one copy of the runtime is loaded, and a context
+    created on torch's device memory works (with the system copy loaded
+    beside torch's, wino_create failed with WINO_ERR_HIP)."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = ("import paper_2605_16941_amd as P\n"
+            "import torch\n"
+            "import wino_inputs as wi\n"
+            "cfg = wi.preset('tiny')\n"
+            "P.WinoModel(cfg, wi.model_weights(cfg, seed=0, device='cuda'), 1, 112).close()\n"
+            "print('runtimes', len({l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l}))\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=240)
+    assert r.returncode == 0, r.stderr[-2000:]
+    assert "runtimes 1" in r.stdout, r.stdout
+
+
 def test_fp16_copies_reject_weights_beyond_fp16_range(P):
     """wino_create in fp16 mode refuses weights with no finite fp16 copy (a
     value beyond 65504 in any multiplied matrix) and accepts the largest bf16
