@@ -142,6 +142,25 @@ def test_mask_id_holding_the_row_max_teacher_forced(P):
     assert worst_dp <= 3 * worst_delta + 1e-4
 
 
+@pytest.mark.parametrize("act", [0, 1], ids=["bf16", "fp16"])
+@pytest.mark.parametrize("variant,tau1,tau2", [("midmask", 0.7, 0.9), ("wide", 0.5, 0.9)])
+def test_contract_other_weights(P, variant, tau1, tau2, act):
+    """The teacher-forced contract on other weights and prompts (weight seed
+    9, the seed of a wider sweep where fp16 moved probabilities furthest,
+    1.2e-3): fp16 at margin 1e-3, bf16 at max(1e-3, 3*delta); decisions
+    compared, with re-masks among them."""
+    got, seen, worst_dp, worst_delta, _ = teacher_forced(P, variant, tau1, tau2, seed=9, tok_seed=59,
+                                                         delta_margin=(act == 0), act=act)
+    n = sum(v for k, v in got.items() if k != "verify_keep")
+    print(f"seed 9 {variant} tau {tau1}/{tau2} act {act}: compared {n} {got}; GPU |dp| vs float64 "
+          f"{worst_dp:.2e}, delta {worst_delta:.2e}")
+    assert n >= 128 and got["remask"] >= 5
+    if act == 0:
+        assert worst_dp <= 3 * worst_delta + 1e-4
+    else:
+        assert worst_dp < 2e-3
+
+
 @pytest.mark.parametrize("variant,tau1,tau2", [("midmask", 0.7, 0.9), ("wide", 0.7, 0.9), ("wide", 0.5, 0.9),
                                                ("literal", 0.7, 0.9)])
 def test_contract_fp16_activations(P, variant, tau1, tau2):
