@@ -21,7 +21,8 @@
  * - No entry point aborts or prints.  Arguments are validated on the host
  *   before any GPU work is enqueued; failures return a negative wino_status
  *   and leave outputs untouched.  HIP runtime failures return WINO_ERR_HIP;
- *   the text is available from wino_last_error(ctx).
+ *   the text is available from wino_last_error(ctx), and for a failed
+ *   wino_create (no context) from wino_last_error(NULL) on the same thread.
  * - A context is not thread-safe; calls that overlap on one context race.
  * - Device pointers must come from the HIP runtime the library is loaded
  *   against.  A process with two copies of the runtime (the system's and one
@@ -53,7 +54,7 @@ typedef enum {
   WINO_ERR_HIP = -3,         /* a HIP runtime call failed                     */
   WINO_ERR_NO_MEMORY = -4,   /* workspace allocation failed                   */
   WINO_ERR_STEP_CAP = -5,    /* a block hit its step cap with cap fill off    */
-  WINO_ERR_UNSUPPORTED = -6  /* model shape the library has no kernels for    */
+  WINO_ERR_UNSUPPORTED = -6  /* shape (or fp16 weight) it has no kernels for  */
 } wino_status;
 
 typedef struct wino_ctx wino_ctx;

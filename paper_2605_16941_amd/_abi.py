@@ -169,8 +169,9 @@ def wino_workspace_bytes(cfg: wino_model_config, max_batch: int, max_seq: int) -
 
 def wino_create(cfg: wino_model_config, weights: wino_weights, max_batch: int, max_seq: int) -> int:
     out = C.c_void_p()
-    _check(lib.wino_create(C.byref(cfg), C.byref(weights), max_batch, max_seq, C.byref(out)),
-           "wino_create")
+    s = lib.wino_create(C.byref(cfg), C.byref(weights), max_batch, max_seq, C.byref(out))
+    if s != 0:
+        raise WinoError(s, "wino_create", lib.wino_last_error(None).decode())
     return out.value
 
 

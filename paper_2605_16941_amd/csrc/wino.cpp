@@ -483,6 +483,17 @@ hipError_t noalloc_scratch(void** out) {
   return hipSuccess;
 }
 
+// Message of the last wino_create failure on this thread (no context exists
+// to hold it); wino_last_error(NULL) returns it.
+thread_local std::string t_create_err;
+
+wino_status create_fail(wino_ctx* c, wino_status s, const char* what, hipError_t e = hipSuccess) {
+  t_create_err = what;
+  if (e != hipSuccess) t_create_err += std::string(": ") + hipGetErrorString(e);
+  if (c) wino_destroy(c);
+  return s;
+}
+
 }  // namespace
 
 extern "C" {
@@ -494,17 +505,17 @@ size_t wino_workspace_bytes(const wino_model_config* cfg, int32_t max_batch, int
 
 wino_status wino_create(const wino_model_config* cfg, const wino_weights* w, int32_t max_batch,
                         int32_t max_seq, wino_ctx** out) {
-  if (!cfg || !w || !out) return WINO_ERR_INVALID_ARG;
+  if (!cfg || !w || !out) return create_fail(nullptr, WINO_ERR_INVALID_ARG, "null argument");
   *out = nullptr;
-  if (max_batch < 1 || max_seq < 2) return WINO_ERR_SHAPE;
-  if (!shape_supported(*cfg)) return WINO_ERR_UNSUPPORTED;
+  if (max_batch < 1 || max_seq < 2) return create_fail(nullptr, WINO_ERR_SHAPE, "max_batch or max_seq");
+  if (!shape_supported(*cfg)) return create_fail(nullptr, WINO_ERR_UNSUPPORTED, "model shape");
   if (!w->tok_emb || !w->attn_norm || !w->w_qkv || !w->w_o || !w->ffn_norm || !w->w_gate_up ||
       !w->w_down || !w->final_norm || !w->lm_head)
-    return WINO_ERR_INVALID_ARG;
+    return create_fail(nullptr, WINO_ERR_INVALID_ARG, "null weight pointer");
   for (int l = 0; l < cfg->n_layers; ++l)
     if (!w->attn_norm[l] || !w->w_qkv[l] || !w->w_o[l] || !w->ffn_norm[l] || !w->w_gate_up[l] ||
         !w->w_down[l])
-      return WINO_ERR_INVALID_ARG;
+      return create_fail(nullptr, WINO_ERR_INVALID_ARG, "null weight pointer");
 
   wino_ctx* c = new wino_ctx();
   c->cfg = *cfg;
@@ -526,16 +537,20 @@ wino_status wino_create(const wino_model_config* cfg, const wino_weights* w, int
 
   // an optional cap on the workspace (bytes), checked before any HIP call
   const char* lim = std::getenv("WINO_WORKSPACE_LIMIT");
-  if (lim && std::strtoull(lim, nullptr, 10) < c->L.total) { delete c; return WINO_ERR_NO_MEMORY; }
-  if (hipGetDevice(&c->device) != hipSuccess) { delete c; return WINO_ERR_HIP; }
-  if (hipMalloc(&c->ws, c->L.total) != hipSuccess) { c->ws = nullptr; delete c; return WINO_ERR_NO_MEMORY; }
-  if (hipHostMalloc(reinterpret_cast<void**>(&c->h_pinned), sizeof(int32_t) * 4 * max_batch) != hipSuccess) {
-    hipFree(c->ws);
-    delete c;
-    return WINO_ERR_NO_MEMORY;
+  if (lim && std::strtoull(lim, nullptr, 10) < c->L.total)
+    return create_fail(c, WINO_ERR_NO_MEMORY, "workspace larger than WINO_WORKSPACE_LIMIT");
+  hipError_t e = hipGetDevice(&c->device);
+  if (e != hipSuccess) return create_fail(c, WINO_ERR_HIP, "hipGetDevice", e);
+  e = hipMalloc(&c->ws, c->L.total);
+  if (e != hipSuccess) { c->ws = nullptr; return create_fail(c, WINO_ERR_NO_MEMORY, "hipMalloc (workspace)", e); }
+  e = hipHostMalloc(reinterpret_cast<void**>(&c->h_pinned), sizeof(int32_t) * 4 * max_batch);
+  if (e != hipSuccess) {
+    c->h_pinned = nullptr;
+    return create_fail(c, WINO_ERR_NO_MEMORY, "hipHostMalloc", e);
   }
   // zeroed workspace: padding columns of the transposed values stay finite
-  if (hipMemset(c->ws, 0, c->L.total) != hipSuccess) { wino_destroy(c); return WINO_ERR_HIP; }
+  e = hipMemset(c->ws, 0, c->L.total);
+  if (e != hipSuccess) return create_fail(c, WINO_ERR_HIP, "hipMemset (workspace)", e);
   // RoPE angles pos * theta^(-2i/hd), in double precision on the host, packed
   // as the QKV epilogue reads them: tab[pos][l][fn] = (cos, sin) of element
   // i = fn*32 + l (the lane of a 32-wide block and its block index)
@@ -551,20 +566,18 @@ wino_status wino_create(const wino_model_config* cfg, const wino_weights* w, int
         t[0] = (float)std::cos(a);
         t[1] = (float)std::sin(a);
       }
-  if (hipMemcpy(c->rope_tab(), tab.data(), tab.size() * 4, hipMemcpyHostToDevice) != hipSuccess) {
-    wino_destroy(c);
-    return WINO_ERR_HIP;
-  }
+  e = hipMemcpy(c->rope_tab(), tab.data(), tab.size() * 4, hipMemcpyHostToDevice);
+  if (e != hipSuccess) return create_fail(c, WINO_ERR_HIP, "hipMemcpy (RoPE table)", e);
   if (cfg->act_precision == WINO_ACT_FP16) {
     // fp16 copies of every matrix the matrix cores multiply (bf16 -> fp16 is
     // exact for |w| >= 2^-17 and moves smaller values by at most 2^-25)
     const size_t d = cfg->d_model, F = cfg->d_ff;
     const size_t per_layer = 3 * d * d + d * d + 2 * F * d + d * F;
     const size_t total = per_layer * cfg->n_layers + (size_t)cfg->vocab * d;
-    if (hipMalloc(&c->wcopy, total * 2) != hipSuccess) {
+    e = hipMalloc(&c->wcopy, total * 2);
+    if (e != hipSuccess) {
       c->wcopy = nullptr;
-      wino_destroy(c);
-      return WINO_ERR_NO_MEMORY;
+      return create_fail(c, WINO_ERR_NO_MEMORY, "hipMalloc (fp16 weight copies)", e);
     }
     c->f16 = 1;
     // the overflow flag lives in the first word of the (zeroed) workspace
@@ -584,17 +597,13 @@ wino_status wino_create(const wino_model_config* cfg, const wino_weights* w, int
     }
     convert(c->lm_head, (size_t)cfg->vocab * d);
     int h_overflow = 0;
-    if (hipGetLastError() != hipSuccess || hipDeviceSynchronize() != hipSuccess ||
-        hipMemcpy(&h_overflow, overflow, sizeof(int), hipMemcpyDeviceToHost) != hipSuccess ||
-        hipMemset(overflow, 0, sizeof(int)) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
-      wino_destroy(c);
-      return WINO_ERR_HIP;
-    }
+    if ((e = hipGetLastError()) != hipSuccess || (e = hipDeviceSynchronize()) != hipSuccess ||
+        (e = hipMemcpy(&h_overflow, overflow, sizeof(int), hipMemcpyDeviceToHost)) != hipSuccess ||
+        (e = hipMemset(overflow, 0, sizeof(int))) != hipSuccess || (e = hipDeviceSynchronize()) != hipSuccess)
+      return create_fail(c, WINO_ERR_HIP, "fp16 weight copies", e);
     // a weight beyond fp16's range has no fp16 copy
-    if (h_overflow) {
-      wino_destroy(c);
-      return WINO_ERR_UNSUPPORTED;
-    }
+    if (h_overflow)
+      return create_fail(c, WINO_ERR_UNSUPPORTED, "a weight matrix holds a value with no finite fp16 copy");
   }
   *out = c;
   return WINO_OK;
@@ -909,6 +918,6 @@ const char* wino_status_string(wino_status s) {
   return "unknown status";
 }
 
-const char* wino_last_error(const wino_ctx* c) { return c ? c->err.c_str() : ""; }
+const char* wino_last_error(const wino_ctx* c) { return c ? c->err.c_str() : t_create_err.c_str(); }
 
 }  // extern "C"

@@ -4,6 +4,7 @@
 // runs without a GPU.  Exits non-zero on the first failed check.
 #include <cmath>
 #include <cstdio>
+#include <cstring>
 #include <cstdlib>
 #include <vector>
 
@@ -51,6 +52,7 @@ int main() {
   wino_weights w{};
   CHECK(wino_create(nullptr, &w, 1, 112, &ctx) == WINO_ERR_INVALID_ARG);
   CHECK(wino_create(&cfg, &w, 0, 112, &ctx) == WINO_ERR_SHAPE);
+  CHECK(std::strcmp(wino_last_error(nullptr), "max_batch or max_seq") == 0);
   wino_model_config bad = cfg;
   bad.head_dim = 96; bad.d_model = 384;
   CHECK(wino_create(&bad, &w, 1, 112, &ctx) == WINO_ERR_UNSUPPORTED);
@@ -119,7 +121,8 @@ int main() {
   for (int s = -7; s <= 0; ++s) CHECK(wino_status_string(static_cast<wino_status>(s)) != nullptr);
   CHECK(wino_kernel_class_name(-1)[0] == 0 && wino_kernel_class_name(WINO_N_KERNEL_CLASSES)[0] == 0);
   for (int k = 0; k < WINO_N_KERNEL_CLASSES; ++k) CHECK(wino_kernel_class_name(k)[0] != 0);
-  CHECK(wino_last_error(nullptr)[0] == 0);
+  // the last failed wino_create on this thread (the workspace-limit case above)
+  CHECK(std::strcmp(wino_last_error(nullptr), "workspace larger than WINO_WORKSPACE_LIMIT") == 0);
 
   std::printf("host checks ok: %d\n", g_checks);
   return 0;

@@ -78,8 +78,10 @@ def test_create_rejects_bad_arguments_before_gpu_work(abi):
     assert abi.lib.wino_create(C.byref(bad), C.byref(w), 1, 112, C.byref(out)) == -6
     bad = tiny_cfg(abi, vocab=4000)
     assert abi.lib.wino_create(C.byref(bad), C.byref(w), 1, 112, C.byref(out)) == -6
+    assert abi.lib.wino_last_error(None) == b"model shape"
     # supported shape, but null weight pointers
     assert abi.lib.wino_create(C.byref(cfg), C.byref(w), 1, 112, C.byref(out)) == -1
+    assert abi.lib.wino_last_error(None) == b"null weight pointer"
     assert out.value is None
 
 
